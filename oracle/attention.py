@@ -1,0 +1,227 @@
+"""fp64 CPU oracle for packed variable-length softmax attention and its gradient.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import or call this
+module: only the tests, the smoke check and the benchmark's CPU-baseline leg
+use it.  It shares no code with the HIP library.
+
+What it computes is the plain definition of scaled dot-product attention,
+Eq. (2) of the problem formulation (section 3):  A = Softmax(Q K^T / sqrt(d)) V,
+applied per head to every packed segment, plus the exact calculus gradient of
+that expression.  The paper leaves several points open; the readings taken
+here are:
+  * d is the head dimension h/n (Table 1 has no d; Table 4 gives h and n), and
+    the softmax scale is passed in explicitly (1/sqrt(d) by default).
+  * causal: key j is visible to query i iff j <= i, both inside the same
+    segment; non-causal: every key of the segment is visible.
+  * segments never attend to each other (packed batch = block-diagonal mask);
+    the paper's b x s layout is the special case of equal lengths.
+  * grouped heads (more query heads than key/value heads) use contiguous
+    groups: query head h reads key/value head h // (Hq / Hkv); dK and dV sum
+    over the group.
+  * LSE is the natural-log log-sum-exp of the scaled logits of each row,
+    laid out [Hq, T].  No dropout, no bias, no gradient flows into LSE.
+
+Everything is float64.  Inputs are expected as float64 arrays holding the
+bf16 values exactly (bf16 -> fp64 widening is exact), so any difference to a
+device result is the device's own rounding.
+
+Rows are processed in blocks of `row_block` query rows: each block is the
+full definition for those rows (all visible keys at once, two-pass softmax),
+so blocking changes nothing but memory use.
+"""
+from __future__ import annotations
+
+from typing import Iterable, List, Sequence, Tuple
+
+import numpy as np
+
+
+def segments(cu_seqlens: Sequence[int]) -> List[Tuple[int, int]]:
+    cu = [int(x) for x in cu_seqlens]
+    return [(cu[i], cu[i + 1]) for i in range(len(cu) - 1)]
+
+
+def _visible_keys(a: int, b: int, r0: int, r1: int, causal: bool) -> int:
+    """Number of keys (from segment start a) any row in [r0, r1) may see."""
+    return (r1 - a) if causal else (b - a)
+
+
+def _logits(qr: np.ndarray, kk: np.ndarray, a: int, r0: int, causal: bool,
+            scale: float) -> np.ndarray:
+    """S[i, j] = scale * <q_i, k_j>, with -inf where key j is not visible.
+    qr: [R, d] rows r0..r0+R-1; kk: [n, d] keys a..a+n-1."""
+    s = scale * (qr @ kk.T)
+    if causal:
+        rows = np.arange(r0, r0 + qr.shape[0])[:, None]
+        cols = np.arange(a, a + kk.shape[0])[None, :]
+        s = np.where(cols <= rows, s, -np.inf)
+    return s
+
+
+def _softmax_stats(s: np.ndarray):
+    """Two-pass log-sum-exp per row; returns (lse, P)."""
+    m = np.max(s, axis=1)
+    lse = m + np.log(np.sum(np.exp(s - m[:, None]), axis=1))
+    p = np.exp(s - lse[:, None])
+    return lse, p
+
+
+def forward(q, k, v, cu_seqlens, causal: bool, scale: float, row_block: int = 256):
+    """O [T, Hq, d] and LSE [Hq, T] (natural log) per Eq. (2)."""
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    g = Hq // Hkv
+    o = np.zeros((T, Hq, v.shape[2]), dtype=np.float64)
+    lse = np.zeros((Hq, T), dtype=np.float64)
+    for a, b in segments(cu_seqlens):
+        for h in range(Hq):
+            hk = h // g
+            for r0 in range(a, b, row_block):
+                r1 = min(b, r0 + row_block)
+                n = _visible_keys(a, b, r0, r1, causal)
+                kk = k[a:a + n, hk]
+                vv = v[a:a + n, hk]
+                s = _logits(q[r0:r1, h], kk, a, r0, causal, scale)
+                l, p = _softmax_stats(s)
+                lse[h, r0:r1] = l
+                o[r0:r1, h] = p @ vv
+    return o, lse
+
+
+def backward(q, k, v, do, cu_seqlens, causal: bool, scale: float, row_block: int = 256):
+    """Gradient of L = sum(dO * O) with O from Eq. (2).
+
+    Returns (O, LSE, dQ, dK, dV), all float64.  With P = softmax(S) and
+    S = scale * Q K^T:
+        dV = P^T dO
+        dP = dO V^T
+        dS = P * (dP - D),  D_i = <dO_i, O_i>   (softmax Jacobian)
+        dQ = scale * dS K,  dK = scale * dS^T Q
+    dK and dV of a key/value head sum the contributions of its query heads.
+    """
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    g = Hq // Hkv
+    o, lse = forward(q, k, v, cu_seqlens, causal, scale, row_block)
+    dq = np.zeros_like(q, dtype=np.float64)
+    dk = np.zeros_like(k, dtype=np.float64)
+    dv = np.zeros_like(v, dtype=np.float64)
+    for a, b in segments(cu_seqlens):
+        for h in range(Hq):
+            hk = h // g
+            for r0 in range(a, b, row_block):
+                r1 = min(b, r0 + row_block)
+                n = _visible_keys(a, b, r0, r1, causal)
+                kk = k[a:a + n, hk]
+                vv = v[a:a + n, hk]
+                s = _logits(q[r0:r1, h], kk, a, r0, causal, scale)
+                p = np.exp(s - lse[h, r0:r1, None])
+                dor = do[r0:r1, h]
+                D = np.sum(dor * o[r0:r1, h], axis=1)
+                dp = dor @ vv.T
+                ds = p * (dp - D[:, None])
+                dq[r0:r1, h] = scale * (ds @ kk)
+                dk[a:a + n, hk] += scale * (ds.T @ q[r0:r1, h])
+                dv[a:a + n, hk] += p.T @ dor
+    return o, lse, dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# Sampled mode: exact values for chosen rows / key columns at any size.
+# Every function below evaluates the same definition as forward()/backward()
+# for a subset of outputs; row results only need that row's visible keys,
+# column results need the statistics (LSE, D) of every row that sees the key.
+# ---------------------------------------------------------------------------
+def _segment_of(cu: np.ndarray, idx: np.ndarray) -> np.ndarray:
+    return np.searchsorted(cu, idx, side="right") - 1
+
+
+def rows_forward_backward(q, k, v, do, cu_seqlens, causal: bool, scale: float,
+                          heads: Iterable[int], rows: Sequence[int]):
+    """For each query head in `heads` and each token index in `rows`:
+    O_i [len(rows), d], LSE_i, dQ_i.  Inputs are [T, H, d] arrays, or objects
+    with `num_heads` and a `head(h)` method returning the [T, d] float64 slice
+    of head h (so large inputs can be widened one head at a time).
+
+    Returns dict head -> (o, lse, dq) with arrays over `rows` (sorted order of
+    the given list is preserved)."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    rows = np.asarray(rows, dtype=np.int64)
+    seg = _segment_of(cu, rows)
+    Hq = _nheads(q)
+    Hkv = _nheads(k)
+    g = Hq // Hkv
+    out = {}
+    for h in heads:
+        hk = h // g
+        qh, kh, vh, doh = _head(q, h), _head(k, hk), _head(v, hk), _head(do, h)
+        o = np.zeros((len(rows), vh.shape[1]))
+        lse = np.zeros(len(rows))
+        dq = np.zeros((len(rows), qh.shape[1]))
+        for si in np.unique(seg):
+            a, b = int(cu[si]), int(cu[si + 1])
+            sel = np.nonzero(seg == si)[0]
+            r = rows[sel]
+            n = (int(r.max()) + 1 - a) if causal else (b - a)
+            kk, vv = kh[a:a + n], vh[a:a + n]
+            s = scale * (qh[r] @ kk.T)
+            if causal:
+                s = np.where(np.arange(a, a + n)[None, :] <= r[:, None], s, -np.inf)
+            l, p = _softmax_stats(s)
+            orow = p @ vv
+            D = np.sum(doh[r] * orow, axis=1)
+            ds = p * (doh[r] @ vv.T - D[:, None])
+            o[sel], lse[sel], dq[sel] = orow, l, scale * (ds @ kk)
+        out[h] = (o, lse, dq)
+    return out
+
+
+def cols_backward(q, k, v, do, cu_seqlens, causal: bool, scale: float,
+                  kv_heads: Iterable[int], seg_index: int, col_lo: int,
+                  row_block: int = 512):
+    """dK_j, dV_j for key columns j in [col_lo, b) of segment `seg_index`
+    (b = segment end), summed over the query heads of each key/value head.
+    Every row that sees one of these keys contributes; with causal masking
+    these are rows i >= col_lo only, so a tail window is cheap at any length.
+    Returns dict kv_head -> (dk [b-col_lo, d], dv [b-col_lo, d])."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    a, b = int(cu[seg_index]), int(cu[seg_index + 1])
+    Hq, Hkv = _nheads(q), _nheads(k)
+    g = Hq // Hkv
+    out = {}
+    for hk in kv_heads:
+        kh, vh = _head(k, hk), _head(v, hk)
+        dk = np.zeros((b - col_lo, kh.shape[1]))
+        dv = np.zeros((b - col_lo, vh.shape[1]))
+        r_start = col_lo if causal else a
+        for h in range(hk * g, (hk + 1) * g):
+            qh, doh = _head(q, h), _head(do, h)
+            for r0 in range(r_start, b, row_block):
+                r1 = min(b, r0 + row_block)
+                n = (r1 - a) if causal else (b - a)
+                kk, vv = kh[a:a + n], vh[a:a + n]
+                s = _logits(qh[r0:r1], kk, a, r0, causal, scale)
+                l, p = _softmax_stats(s)
+                orow = p @ vv
+                dor = doh[r0:r1]
+                D = np.sum(dor * orow, axis=1)
+                ds = p * (dor @ vv.T - D[:, None])
+                c0 = col_lo - a
+                dk[: n - c0] += scale * (ds[:, c0:n].T @ qh[r0:r1])
+                dv[: n - c0] += p[:, c0:n].T @ dor
+        out[hk] = (dk, dv)
+    return out
+
+
+def _nheads(x) -> int:
+    if hasattr(x, "num_heads"):
+        return x.num_heads
+    return x.shape[1]
+
+
+def _head(x, h):
+    """[T, d] float64 view of head h; `x` is an array [T, H, d] or an object
+    with a `head(h)` method returning that slice."""
+    if hasattr(x, "head"):
+        return x.head(h)
+    return np.asarray(x[:, h], dtype=np.float64)
