@@ -1,0 +1,110 @@
+/*
+ * pdyattn -- packed variable-length softmax attention, forward and backward,
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The operation is scaled dot-product attention as written in Eq. (2) of the
+ * problem formulation (section 3):  A = Softmax(Q K^T / sqrt(d)) V, applied per
+ * head to a packed batch of dynamic-length sequences laid out as in the
+ * tensor-layout specification (Table 2, section 4.2: activations b x s/p x h,
+ * here packed to [T, H, d] with segment offsets).  The backward computes the
+ * gradient of that expression, which the training workloads of section 5.1
+ * need.  Readings of points the paper leaves open:
+ *   - d is the head dimension (h/n of Table 4); the scale is an argument.
+ *   - segments never attend to each other; with causal = 1 key j is visible
+ *     to query i iff j <= i within the segment.
+ *   - grouped heads: query head h reads key/value head h / (Hq / Hkv).
+ *   - lse is the natural-log log-sum-exp of the scaled logits, [Hq, T].
+ *
+ * Conventions shared by every entry point:
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates or frees device memory.  Dense, row-major, last dim
+ *     contiguous, 16-byte aligned.  bf16 tensors are raw IEEE bfloat16 bits.
+ *   - cu_seqlens is an int32 device array of num_seqs + 1 offsets with
+ *     cu[0] = 0, cu[i] <= cu[i+1], cu[num_seqs] = total_tokens.  Zero-length
+ *     segments are allowed.  Its contents are trusted (reading them on the
+ *     host would force a synchronisation); attn_validate_cu_seqlens checks it.
+ *   - max_seqlen must be >= every segment length (an upper bound suffices).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream) and
+ *     the call returns without synchronising.  Outputs are fully overwritten.
+ *   - Argument errors are reported before anything is launched.  A non-OK
+ *     status leaves a thread-local message in pdy_last_error().
+ *   - Scratch memory comes from the caller's `workspace` (16-byte aligned,
+ *     at least the size the matching *_workspace_size query returns).
+ *   - Calls on different streams with disjoint outputs and workspaces may run
+ *     concurrently; the library holds no global state besides the per-thread
+ *     error message.
+ *   - Results are bitwise reproducible run to run (no atomics feed outputs).
+ */
+#ifndef PDYATTN_H
+#define PDYATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PDY_OK = 0,
+  PDY_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad size or flag          */
+  PDY_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}                            */
+  PDY_ERR_WORKSPACE = -3,   /* workspace smaller than the query function asks for */
+  PDY_ERR_HIP = -4          /* a HIP runtime call failed (message has the detail) */
+} pdy_status;
+
+/* Bytes of workspace attn_fwd needs for these sizes (>= 256).  Returns 0 when
+ * the sizes are invalid. */
+size_t attn_fwd_workspace_size(int32_t total_tokens, int32_t num_seqs, int32_t max_seqlen,
+                               int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim);
+
+/* Bytes of workspace attn_bwd needs (it holds D = rowsum(dO * O), fp32
+ * [Hq, T], plus the tile schedule).  Returns 0 when the sizes are invalid. */
+size_t attn_bwd_workspace_size(int32_t total_tokens, int32_t num_seqs, int32_t max_seqlen,
+                               int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim);
+
+/* Forward of Eq. (2) (section 3) over a packed batch.
+ *   q   bf16 [T, Hq,  d]        k, v  bf16 [T, Hkv, d]
+ *   o   bf16 [T, Hq,  d] (out)  lse   fp32 [Hq, T]    (out, natural log)
+ *   num_heads_q % num_heads_kv == 0;  head_dim in {64, 128};  causal in {0, 1};
+ *   scale finite and > 0 (usually 1/sqrt(head_dim)).
+ * T = 0 is a no-op.  o and lse must not alias the inputs. */
+pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                    int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen,
+                    int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                    int32_t causal, float scale,
+                    void* o, float* lse,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of Eq. (2) (section 3): gradients of sum(dout * o).
+ *   q, o, dout bf16 [T, Hq, d];  k, v bf16 [T, Hkv, d];  lse fp32 [Hq, T] as
+ *   written by attn_fwd for the same inputs.
+ *   dq fp32 [T, Hq, d] (out);  dk, dv fp32 [T, Hkv, d] (out; with grouped
+ *   heads each sums its query heads).  Gradients are fp32 so that large
+ *   accumulated values keep their precision.
+ * Same size/flag rules as attn_fwd. */
+pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                    const void* dout, const int32_t* cu_seqlens,
+                    int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen,
+                    int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                    int32_t causal, float scale,
+                    float* dq, float* dk, float* dv,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Debug helper: copies cu_seqlens to the host (synchronising `stream`) and
+ * checks cu[0] = 0, monotonicity and cu[num_seqs] = total_tokens.  On success
+ * writes the longest segment length to *max_seqlen_out (may be NULL). */
+pdy_status attn_validate_cu_seqlens(const int32_t* cu_seqlens, int32_t num_seqs,
+                                    int32_t total_tokens, int32_t* max_seqlen_out,
+                                    void* stream);
+
+/* Static text for a status code. */
+const char* pdy_status_string(int32_t status);
+
+/* Detail of the last non-OK status returned on this thread ("" if none). */
+const char* pdy_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PDYATTN_H */

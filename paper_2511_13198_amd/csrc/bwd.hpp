@@ -1,0 +1,376 @@
+// Backward of Eq. (2) (section 3), recomputing the probabilities from the
+// saved log-sum-exp instead of storing them.  With S = scale * Q K^T,
+// P = exp(S - LSE), D_i = <dO_i, O_i>:
+//   dV = P^T dO,  dP = dO V^T,  dS = P * (dP - D),  dK = scale * dS^T Q,
+//   dQ = scale * dS K.
+// Three kernels:
+//   * bwd_pre_kernel    D = rowsum(dO * O) (fp32, [Hq, T]) -- bandwidth bound.
+//   * bwd_dkdv_kernel   one workgroup per (segment, kv head, 128-key tile); the
+//                       waves own 32 keys each, keep K and V in registers and
+//                       dK^T / dV^T in accumulators, and sweep every query
+//                       head of the group and every query tile that sees the
+//                       keys.  Written once, no atomics.
+//   * bwd_dq_kernel     one workgroup per (segment, query head, 128-row tile);
+//                       mirrors the forward: recomputes S^T and dP^T, forms
+//                       dS^T and accumulates dQ^T = K^T dS^T.  No atomics.
+// All outputs are deterministic.
+#pragma once
+#include "common.hpp"
+
+namespace pdy {
+
+// D[h][i] = sum_d dO[i,h,d] * O[i,h,d]; one 16-lane group per (row, head).
+template <int D>
+__global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict__ o,
+                                                      const uint16_t* __restrict__ dout,
+                                                      float* __restrict__ dd, int total_tokens,
+                                                      int hq) {
+  constexpr int LANES = D / 8;  // 16 B per lane
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t pair = gid / LANES;  // (row, head) flattened as row * hq + h
+  const int sub = (int)(gid % LANES);
+  const size_t npairs = (size_t)total_tokens * hq;
+  float acc = 0.f;
+  if (pair < npairs) {
+    const u32x4 ov = *reinterpret_cast<const u32x4*>(o + pair * D + sub * 8);
+    const u32x4 gv = *reinterpret_cast<const u32x4*>(dout + pair * D + sub * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc += __uint_as_float(ov[i] << 16) * __uint_as_float(gv[i] << 16);
+      acc += __uint_as_float(ov[i] & 0xffff0000u) * __uint_as_float(gv[i] & 0xffff0000u);
+    }
+  }
+#pragma unroll
+  for (int off = LANES / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, LANES);
+  if (pair < npairs && sub == 0) {
+    const size_t row = pair / hq;
+    const int h = (int)(pair % hq);
+    dd[(size_t)h * total_tokens + row] = acc;
+  }
+}
+
+struct BwdArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const uint16_t* dout;
+  const float* lse;  // natural log, [Hq, T]
+  const float* dd;   // [Hq, T]
+  const int32_t* cu;
+  float* dq;
+  float* dk;
+  float* dv;
+  Plan plan;
+  int total_tokens;
+  int hq;
+  int hkv;
+  int causal;
+  float scale;
+  float scale_log2;
+};
+
+template <int D>
+struct DkdvCfg {
+  static constexpr int BK = 128;  // keys per workgroup (32 per wave)
+  static constexpr int BQ = 64;   // query rows per step
+  static constexpr int NW = 4;
+  static constexpr int NT = NW * 64;
+  static constexpr int PITCH = D + 8;
+  static constexpr int TILE = BQ * PITCH;
+  // per stage: Q tile, dO tile, lse2[BQ], D[BQ]
+  static constexpr int STAGE = 2 * TILE * 2 + 2 * BQ * 4;
+  static constexpr int LDS_BYTES = 2 * STAGE;
+};
+
+template <int D>
+__global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
+  using C = DkdvCfg<D>;
+  constexpr int BK = C::BK, BQ = C::BQ, PITCH = C::PITCH;
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+
+  const int item = blockIdx.x / a.hkv;
+  const int hk = blockIdx.x % a.hkv;
+  int seg, level;
+  if (!plan_lookup(a.plan, item, seg, level)) return;
+  const int seg_lo = a.cu[seg];
+  const int seg_hi = a.cu[seg + 1];
+  const int nt = (seg_hi - seg_lo + BK - 1) / BK;
+  const int ktile = nt - 1 - level;
+  const int k0 = seg_lo + ktile * BK;
+  const int g = a.hq / a.hkv;
+
+  const int l = __lane_id();
+  const int w = threadIdx.x >> 6;
+  const int hh = l >> 5;
+  const int kw0 = k0 + w * 32;         // first key of this wave
+  const int key = kw0 + (l & 31);      // this lane's key
+  const size_t qstride = (size_t)a.hq * D;
+  const size_t kvstride = (size_t)a.hkv * D;
+
+  // K^T and V^T as B operands: lane holds K[key][ks*16 + hh*8 + j]
+  bf16x8 kf[D / 16], vf[D / 16];
+  {
+    const bool ok = key < seg_hi;
+    const uint16_t* kp = a.k + (size_t)key * kvstride + (size_t)hk * D + hh * 8;
+    const uint16_t* vp = a.v + (size_t)key * kvstride + (size_t)hk * D + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      kf[ks] = load_bf16x8(kp + ks * 16, ok);
+      vf[ks] = load_bf16x8(vp + ks * 16, ok);
+    }
+  }
+  f32x16 dka[D / 32], dva[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) {
+    dka[i] = zero16();
+    dva[i] = zero16();
+  }
+
+  // query rows that can see this key tile
+  const int qstart = a.causal ? k0 : seg_lo;
+  const int nqt = (seg_hi - qstart + BQ - 1) / BQ;
+  const int nsteps = nqt * g;
+
+  auto stage_ptr = [&](int buf) { return reinterpret_cast<uint8_t*>(smem) + buf * C::STAGE; };
+
+  TileLoader<BQ, D, C::NT> ql, gl;
+  float lse_r = 0.f, dd_r = 0.f;  // one row per thread (threads 0..BQ-1)
+  auto issue = [&](int step) {
+    const int hi = step / nqt;
+    const int qi = step % nqt;
+    const int h = hk * g + hi;
+    const int r0 = qstart + qi * BQ;
+    ql.load(a.q + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
+    gl.load(a.dout + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
+    if (threadIdx.x < BQ) {
+      const int r = r0 + threadIdx.x;
+      const bool ok = r < seg_hi;
+      lse_r = ok ? a.lse[(size_t)h * a.total_tokens + r] * kLog2e : 0.f;
+      dd_r = ok ? a.dd[(size_t)h * a.total_tokens + r] : 0.f;
+    }
+  };
+  auto commit = [&](int buf) {
+    uint8_t* st = stage_ptr(buf);
+    ql.store(reinterpret_cast<uint16_t*>(st), PITCH);
+    gl.store(reinterpret_cast<uint16_t*>(st) + C::TILE, PITCH);
+    float* stats = reinterpret_cast<float*>(st + 2 * C::TILE * 2);
+    if (threadIdx.x < BQ) {
+      stats[threadIdx.x] = lse_r;
+      stats[BQ + threadIdx.x] = dd_r;
+    }
+  };
+
+  if (nsteps > 0) {
+    issue(0);
+    commit(0);
+  }
+  for (int step = 0; step < nsteps; ++step) {
+    const bool more = step + 1 < nsteps;
+    if (more) issue(step + 1);
+    __syncthreads();
+    const uint8_t* st = stage_ptr(step & 1);
+    const uint16_t* qs = reinterpret_cast<const uint16_t*>(st);
+    const uint16_t* gs = qs + C::TILE;
+    const float* lse_s = reinterpret_cast<const float*>(st + 2 * C::TILE * 2);
+    const float* dd_s = lse_s + BQ;
+    const int r0 = qstart + (step % nqt) * BQ;
+
+    const bool active = (kw0 < seg_hi) && (!a.causal || r0 + BQ - 1 >= kw0);
+    if (active) {
+      const bool need_mask = (a.causal && r0 < kw0 + 31) || (r0 + BQ > seg_hi);
+      f32x16 p[BQ / 32], ds[BQ / 32];
+#pragma unroll
+      for (int rb = 0; rb < BQ / 32; ++rb) {
+        // S[row][key] = Q K^T : A = Q rows from LDS, B = K^T registers
+        f32x16 s = zero16();
+        f32x16 dp = zero16();
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          s = mfma32(lds_row_operand(qs, PITCH, rb * 32, ks * 16), kf[ks], s);
+          dp = mfma32(lds_row_operand(gs, PITCH, rb * 32, ks * 16), vf[ks], dp);
+        }
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const int rl = rb * 32 + grp * 8 + hh * 4;  // local row of r = grp*4
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rl);
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(dd_s + rl);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = grp * 4 + e;
+            float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -l4[e]));
+            if (need_mask) {
+              const int row = r0 + rl + e;
+              const bool vis = row < seg_hi && key < seg_hi && (!a.causal || key <= row);
+              if (!vis) pv = 0.f;
+            }
+            p[rb][r] = pv;
+            ds[rb][r] = pv * (dp[r] - d4[e]);
+          }
+        }
+      }
+      // dV^T += dO^T P  and  dK^T += Q^T dS  over 4 row steps of 16
+#pragma unroll
+      for (int t = 0; t < BQ / 16; ++t) {
+        bf16x8 pb = pack8(p[t >> 1], (t & 1) * 8);
+        bf16x8 sb = pack8(ds[t >> 1], (t & 1) * 8);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          dva[db] = mfma32(lds_tr_a_operand(gs, PITCH, t * 16, db * 32), pb, dva[db]);
+          dka[db] = mfma32(lds_tr_a_operand(qs, PITCH, t * 16, db * 32), sb, dka[db]);
+        }
+      }
+    }
+    if (more) commit((step + 1) & 1);
+  }
+
+  if (key < seg_hi) {
+    float* dkp = a.dk + (size_t)key * kvstride + (size_t)hk * D;
+    float* dvp = a.dv + (size_t)key * kvstride + (size_t)hk * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int d0 = db * 32 + grp * 8 + hh * 4;
+        f32x4 kv = {dka[db][grp * 4] * a.scale, dka[db][grp * 4 + 1] * a.scale,
+                    dka[db][grp * 4 + 2] * a.scale, dka[db][grp * 4 + 3] * a.scale};
+        f32x4 vv = {dva[db][grp * 4], dva[db][grp * 4 + 1], dva[db][grp * 4 + 2],
+                    dva[db][grp * 4 + 3]};
+        *reinterpret_cast<f32x4*>(dkp + d0) = kv;
+        *reinterpret_cast<f32x4*>(dvp + d0) = vv;
+      }
+  }
+}
+
+template <int D>
+struct DqCfg {
+  static constexpr int BQ = 128;
+  static constexpr int BK = 64;
+  static constexpr int NW = 4;
+  static constexpr int NT = NW * 64;
+  static constexpr int PITCH = D + 8;
+  static constexpr int TILE = BK * PITCH;
+  static constexpr int LDS_BYTES = 2 * 2 * TILE * 2;
+};
+
+template <int D>
+__global__ void __launch_bounds__(256, 1) bwd_dq_kernel(BwdArgs a) {
+  using C = DqCfg<D>;
+  constexpr int BQ = C::BQ, BK = C::BK, PITCH = C::PITCH;
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+
+  const int item = blockIdx.x / a.hq;
+  const int h = blockIdx.x % a.hq;
+  int seg, level;
+  if (!plan_lookup(a.plan, item, seg, level)) return;
+  const int seg_lo = a.cu[seg];
+  const int seg_hi = a.cu[seg + 1];
+  const int q0 = seg_lo + level * BQ;
+  const int hk = h / (a.hq / a.hkv);
+
+  const int l = __lane_id();
+  const int w = threadIdx.x >> 6;
+  const int hh = l >> 5;
+  const int row = q0 + w * 32 + (l & 31);
+  const int wrow0 = q0 + w * 32;
+  const int wrow_last = wrow0 + 31;
+  const size_t qstride = (size_t)a.hq * D;
+  const size_t kvstride = (size_t)a.hkv * D;
+
+  bf16x8 qf[D / 16], gf[D / 16];
+  float lse2 = 0.f, ddv = 0.f;
+  {
+    const bool ok = row < seg_hi;
+    const uint16_t* qp = a.q + (size_t)row * qstride + (size_t)h * D + hh * 8;
+    const uint16_t* gp = a.dout + (size_t)row * qstride + (size_t)h * D + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      qf[ks] = load_bf16x8(qp + ks * 16, ok);
+      gf[ks] = load_bf16x8(gp + ks * 16, ok);
+    }
+    if (ok) {
+      lse2 = a.lse[(size_t)h * a.total_tokens + row] * kLog2e;
+      ddv = a.dd[(size_t)h * a.total_tokens + row];
+    }
+  }
+  f32x16 dqa[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) dqa[i] = zero16();
+
+  const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
+  const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
+  // buffer b: K at smem + 2*b*TILE, V right after it
+  auto kbuf = [&](int b) { return smem + 2 * b * C::TILE; };
+  auto vbuf = [&](int b) { return smem + (2 * b + 1) * C::TILE; };
+  TileLoader<BK, D, C::NT> kl, vl;
+  const uint16_t* kbase = a.k + (size_t)hk * D;
+  const uint16_t* vbase = a.v + (size_t)hk * D;
+  if (ntiles > 0) {
+    kl.load(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+    vl.load(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+    kl.store(kbuf(0), PITCH);
+    vl.store(vbuf(0), PITCH);
+  }
+  for (int it = 0; it < ntiles; ++it) {
+    const int k0 = seg_lo + it * BK;
+    const bool more = it + 1 < ntiles;
+    if (more) {
+      const int k1 = k0 + BK;
+      kl.load(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      vl.load(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+    }
+    __syncthreads();
+    const uint16_t* ks_ = kbuf(it & 1);
+    const uint16_t* vs_ = vbuf(it & 1);
+    const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
+    if (active) {
+      const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
+      f32x16 ds[BK / 32];
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb) {
+        f32x16 s = zero16();
+        f32x16 dp = zero16();
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          s = mfma32(lds_row_operand(ks_, PITCH, kb * 32, ks * 16), qf[ks], s);
+          dp = mfma32(lds_row_operand(vs_, PITCH, kb * 32, ks * 16), gf[ks], dp);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -lse2));
+          if (need_mask) {
+            const int key = k0 + kb * 32 + (r >> 2) * 8 + hh * 4 + (r & 3);
+            const bool vis = key < seg_hi && (!a.causal || key <= row);
+            if (!vis) pv = 0.f;
+          }
+          ds[kb][r] = pv * (dp[r] - ddv);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < BK / 16; ++t) {
+        bf16x8 sb = pack8(ds[t >> 1], (t & 1) * 8);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+          dqa[db] = mfma32(lds_tr_a_operand(ks_, PITCH, t * 16, db * 32), sb, dqa[db]);
+      }
+    }
+    if (more) {
+      kl.store(kbuf((it + 1) & 1), PITCH);
+      vl.store(vbuf((it + 1) & 1), PITCH);
+    }
+  }
+
+  if (row < seg_hi) {
+    float* dqp = a.dq + (size_t)row * qstride + (size_t)h * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int d0 = db * 32 + grp * 8 + hh * 4;
+        f32x4 v = {dqa[db][grp * 4] * a.scale, dqa[db][grp * 4 + 1] * a.scale,
+                   dqa[db][grp * 4 + 2] * a.scale, dqa[db][grp * 4 + 3] * a.scale};
+        *reinterpret_cast<f32x4*>(dqp + d0) = v;
+      }
+  }
+}
+
+}  // namespace pdy

@@ -1,0 +1,203 @@
+// Forward of Eq. (2) (section 3): tiled online-softmax attention on the bf16
+// matrix cores of gfx950.
+//
+// One workgroup = one (segment, query head, query tile of 128 rows); each of
+// its 4 waves owns 32 query rows, with Q held in registers as the B operand of
+//   S^T = K Q^T            (32 keys x 32 rows per MFMA tile, keys from LDS)
+// so that each lane owns one query row (l % 32) and half of the keys of a
+// tile; the row max / row sum need one cross-half exchange (permlane32_swap).
+// The probabilities are rounded to bf16 and fed back as the B operand of
+//   O^T += V^T P^T          (32 head-dim x 32 rows per MFMA tile)
+// with V^T read from the row-major LDS tile by transposing reads.  K/V tiles of
+// 64 keys are double-buffered: the global loads of tile t+1 are in flight while
+// tile t is computed.  Tiles entirely above the causal diagonal are never
+// visited; only tiles crossing the diagonal or the segment end are masked.
+// The row statistics are kept in base 2 (log2(e) is folded into the scale) and
+// converted back for the natural-log LSE output.
+#pragma once
+#include "common.hpp"
+
+namespace pdy {
+
+template <int D>
+struct FwdCfg {
+  static constexpr int BQ = 128;
+  static constexpr int BK = 64;
+  static constexpr int NW = 4;
+  static constexpr int NT = NW * 64;
+  static constexpr int PITCH = D + 8;  // LDS row pitch in bf16 elements
+  static constexpr int TILE = BK * PITCH;
+  static constexpr int LDS_BYTES = 2 * 2 * TILE * 2;  // {K, V} x double buffer
+};
+
+struct FwdArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* cu;
+  uint16_t* o;
+  float* lse;
+  Plan plan;
+  int total_tokens;
+  int hq;
+  int hkv;
+  int causal;
+  float scale_log2;  // scale * log2(e)
+};
+
+template <int D>
+__global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
+  using C = FwdCfg<D>;
+  constexpr int BQ = C::BQ, BK = C::BK, PITCH = C::PITCH;
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+
+  const int item = blockIdx.x / a.hq;
+  const int h = blockIdx.x % a.hq;
+  int seg, level;
+  if (!plan_lookup(a.plan, item, seg, level)) return;
+  const int seg_lo = a.cu[seg];
+  const int seg_hi = a.cu[seg + 1];
+  const int q0 = seg_lo + level * BQ;
+  const int hk = h / (a.hq / a.hkv);
+
+  const int l = __lane_id();
+  const int w = threadIdx.x >> 6;
+  const int hh = l >> 5;
+  const int row = q0 + w * 32 + (l & 31);  // this lane's query row
+  const int wrow0 = q0 + w * 32;
+  const int wrow_last = wrow0 + 31;
+
+  const size_t qstride = (size_t)a.hq * D;
+  const size_t kvstride = (size_t)a.hkv * D;
+
+  // Q^T as B operand: lane holds Q[row][ks*16 + hh*8 + j]
+  bf16x8 qf[D / 16];
+  {
+    const bool ok = row < seg_hi;
+    const uint16_t* qp = a.q + (size_t)row * qstride + (size_t)h * D + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = load_bf16x8(qp + ks * 16, ok);
+  }
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) oacc[i] = zero16();
+  float m = -INFINITY;  // running max of scaled logits (base 2)
+  float lsum = 0.f;     // partial row sum over this lane's keys
+
+  const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
+  const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
+
+  // buffer b: K at smem + 2*b*TILE, V right after it
+  auto kbuf = [&](int b) { return smem + 2 * b * C::TILE; };
+  auto vbuf = [&](int b) { return smem + (2 * b + 1) * C::TILE; };
+
+  TileLoader<BK, D, C::NT> kl, vl;
+  const uint16_t* kbase = a.k + (size_t)hk * D;
+  const uint16_t* vbase = a.v + (size_t)hk * D;
+  {
+    const int k0 = seg_lo;
+    kl.load(kbase + (size_t)k0 * kvstride, kvstride, seg_hi - k0);
+    vl.load(vbase + (size_t)k0 * kvstride, kvstride, seg_hi - k0);
+    kl.store(kbuf(0), PITCH);
+    vl.store(vbuf(0), PITCH);
+  }
+
+  for (int it = 0; it < ntiles; ++it) {
+    const int k0 = seg_lo + it * BK;
+    const bool more = it + 1 < ntiles;
+    if (more) {
+      const int k1 = k0 + BK;
+      kl.load(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      vl.load(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+    }
+    __syncthreads();
+    const uint16_t* ks_ = kbuf(it & 1);
+    const uint16_t* vs_ = vbuf(it & 1);
+
+    const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
+    if (active) {
+      // S^T for two 32-key blocks
+      f32x16 s[BK / 32];
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb) {
+        s[kb] = zero16();
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          bf16x8 kf = lds_row_operand(ks_, PITCH, kb * 32, ks * 16);
+          s[kb] = mfma32(kf, qf[ks], s[kb]);
+        }
+      }
+      const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
+      if (need_mask) {
+#pragma unroll
+        for (int kb = 0; kb < BK / 32; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + kb * 32 + (r >> 2) * 8 + hh * 4 + (r & 3);
+            const bool vis = key < seg_hi && (!a.causal || key <= row);
+            if (!vis) s[kb][r] = -INFINITY;
+          }
+      }
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
+      tmax = fmaxf(tmax, partner32(tmax));
+      const float mnew = fmaxf(m, tmax * a.scale_log2);
+      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
+      const float alpha = fast_exp2(m - muse);
+      m = mnew;
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = fast_exp2(__builtin_fmaf(s[kb][r], a.scale_log2, -muse));
+          s[kb][r] = p;
+          psum += p;
+        }
+      lsum = lsum * alpha + psum;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      // O^T += V^T P^T over 4 key steps of 16
+#pragma unroll
+      for (int t = 0; t < BK / 16; ++t) {
+        bf16x8 pf = pack8(s[t >> 1], (t & 1) * 8);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          bf16x8 vf = lds_tr_a_operand(vs_, PITCH, t * 16, db * 32);
+          oacc[db] = mfma32(vf, pf, oacc[db]);
+        }
+      }
+    }
+    if (more) {
+      kl.store(kbuf((it + 1) & 1), PITCH);
+      vl.store(vbuf((it + 1) & 1), PITCH);
+    }
+  }
+
+  // epilogue: normalise, write O (bf16) and LSE (natural log)
+  const float ltot = lsum + partner32(lsum);
+  if (row < seg_hi) {
+    const float inv = 1.f / ltot;
+    uint16_t* op = a.o + (size_t)row * qstride + (size_t)h * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x2 v01 = {oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv};
+        f32x2 v23 = {oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv};
+        bf16x2 b01 = __builtin_convertvector(v01, bf16x2);
+        bf16x2 b23 = __builtin_convertvector(v23, bf16x2);
+        u32x2 pk = {__builtin_bit_cast(uint32_t, b01), __builtin_bit_cast(uint32_t, b23)};
+        *reinterpret_cast<u32x2*>(op + db * 32 + g * 8 + hh * 4) = pk;
+      }
+    if (hh == 0) a.lse[(size_t)h * a.total_tokens + row] = (m + __builtin_log2f(ltot)) * kLn2;
+  }
+}
+
+}  // namespace pdy

@@ -1,0 +1,331 @@
+// C-ABI of the pdyattn library: argument validation, workspace carving and
+// kernel launches.  Declarations and the contract live in include/pdyattn.h.
+#include "../../include/pdyattn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "bwd.hpp"
+#include "fwd.hpp"
+#include "plan.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+pdy_status fail(pdy_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+pdy_status hip_fail(hipError_t e, const char* what) {
+  return fail(PDY_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kTile = 128;  // schedule granularity shared by every kernel
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Sizes {
+  int64_t T, N, maxlen, hq, hkv, d;
+  int max_nt;
+};
+
+pdy_status check_sizes(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv, int32_t d,
+                       Sizes* out) {
+  if (T < 0) return fail(PDY_ERR_INVALID_ARG, "total_tokens must be >= 0 (got %d)", T);
+  if (N < 1) return fail(PDY_ERR_INVALID_ARG, "num_seqs must be >= 1 (got %d)", N);
+  if (maxlen < 0 || maxlen > T)
+    return fail(PDY_ERR_INVALID_ARG, "max_seqlen must be in [0, total_tokens] (got %d, T=%d)",
+                maxlen, T);
+  if (T > 0 && maxlen < 1)
+    return fail(PDY_ERR_INVALID_ARG, "max_seqlen must be >= 1 when total_tokens > 0");
+  if (hq < 1 || hkv < 1)
+    return fail(PDY_ERR_INVALID_ARG, "head counts must be >= 1 (got Hq=%d, Hkv=%d)", hq, hkv);
+  if (hq % hkv != 0)
+    return fail(PDY_ERR_INVALID_ARG, "num_heads_q (%d) must be a multiple of num_heads_kv (%d)",
+                hq, hkv);
+  if (d != 64 && d != 128)
+    return fail(PDY_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d);
+  // element offsets are computed in 64 bits; keep T*H*d well inside that and
+  // the grid (items x heads) inside 2^31 blocks
+  const int64_t items = (int64_t)T / kTile + N;
+  if (items * hq >= (int64_t)1 << 31)
+    return fail(PDY_ERR_INVALID_ARG, "problem too large for one launch");
+  out->T = T;
+  out->N = N;
+  out->maxlen = maxlen;
+  out->hq = hq;
+  out->hkv = hkv;
+  out->d = d;
+  out->max_nt = (int)((maxlen + kTile - 1) / kTile);
+  if (out->max_nt < 1) out->max_nt = 1;
+  return PDY_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t plan_bytes(const Sizes& s) { return align256(pdy::plan_ints((int)s.N, s.max_nt) * 4); }
+
+size_t dd_bytes(const Sizes& s) { return align256((size_t)s.hq * (size_t)s.T * 4); }
+
+pdy::Plan make_plan(int32_t* ws, const Sizes& s) {
+  pdy::Plan p;
+  p.order = ws + s.N;
+  p.start = ws + 2 * s.N + s.max_nt;
+  p.total = ws + 2 * s.N + 2 * s.max_nt;
+  p.max_nt = s.max_nt;
+  return p;
+}
+
+int64_t grid_items(const Sizes& s) {
+  const int64_t bound1 = s.T / kTile + s.N;
+  const int64_t bound2 = s.N * (int64_t)s.max_nt;
+  return bound1 < bound2 ? bound1 : bound2;
+}
+
+template <typename K>
+hipError_t set_lds(K kernel, int bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+}
+
+// One-time per-process kernel attribute setup (LDS above the 64 KiB default).
+hipError_t init_kernels() {
+  static hipError_t status = [] {
+    hipError_t e;
+    if ((e = set_lds(pdy::fwd_kernel<64>, pdy::FwdCfg<64>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::fwd_kernel<128>, pdy::FwdCfg<128>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::bwd_dkdv_kernel<64>, pdy::DkdvCfg<64>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::bwd_dkdv_kernel<128>, pdy::DkdvCfg<128>::LDS_BYTES)) != hipSuccess)
+      return e;
+    if ((e = set_lds(pdy::bwd_dq_kernel<64>, pdy::DqCfg<64>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::bwd_dq_kernel<128>, pdy::DqCfg<128>::LDS_BYTES)) != hipSuccess) return e;
+    return hipSuccess;
+  }();
+  return status;
+}
+
+pdy_status check_scale(float scale, int32_t causal) {
+  if (causal != 0 && causal != 1) return fail(PDY_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(PDY_ERR_INVALID_ARG, "scale must be finite and > 0");
+  return PDY_OK;
+}
+
+pdy_status check_ptr(const void* p, const char* name) {
+  if (p == nullptr) return fail(PDY_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned16(p)) return fail(PDY_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return PDY_OK;
+}
+
+pdy_status launch_plan(const int32_t* cu, int32_t* ws, const Sizes& s, hipStream_t st) {
+  hipLaunchKernelGGL(pdy::plan_kernel, dim3(1), dim3(pdy::kPlanThreads), 0, st, cu, (int)s.N, kTile,
+                     s.max_nt, ws);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "plan_kernel launch");
+  return PDY_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pdy_status_string(int32_t status) {
+  switch (status) {
+    case PDY_OK: return "ok";
+    case PDY_ERR_INVALID_ARG: return "invalid argument";
+    case PDY_ERR_UNSUPPORTED: return "unsupported configuration";
+    case PDY_ERR_WORKSPACE: return "workspace too small";
+    case PDY_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* pdy_last_error(void) { return g_err; }
+
+size_t attn_fwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv,
+                               int32_t d) {
+  Sizes s;
+  if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
+  return plan_bytes(s);
+}
+
+size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv,
+                               int32_t d) {
+  Sizes s;
+  if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
+  return plan_bytes(s) + dd_bytes(s);
+}
+
+pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                    int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen, int32_t num_heads_q,
+                    int32_t num_heads_kv, int32_t head_dim, int32_t causal, float scale, void* o,
+                    float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  Sizes s;
+  pdy_status st;
+  if ((st = check_sizes(total_tokens, num_seqs, max_seqlen, num_heads_q, num_heads_kv, head_dim,
+                        &s)) != PDY_OK)
+    return st;
+  if ((st = check_scale(scale, causal)) != PDY_OK) return st;
+  if (s.T == 0) return PDY_OK;
+  if ((st = check_ptr(q, "q")) || (st = check_ptr(k, "k")) || (st = check_ptr(v, "v")) ||
+      (st = check_ptr(o, "o")) || (st = check_ptr(lse, "lse")) ||
+      (st = check_ptr(workspace, "workspace")))
+    return st;
+  if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
+    return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
+  const size_t need = plan_bytes(s);
+  if (workspace_bytes < need)
+    return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, attn_fwd needs %zu", workspace_bytes,
+                need);
+  hipError_t e = init_kernels();
+  if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  int32_t* ws = reinterpret_cast<int32_t*>(workspace);
+  if ((st = launch_plan(cu_seqlens, ws, s, hs)) != PDY_OK) return st;
+
+  pdy::FwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.cu = cu_seqlens;
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.plan = make_plan(ws, s);
+  a.total_tokens = (int)s.T;
+  a.hq = (int)s.hq;
+  a.hkv = (int)s.hkv;
+  a.causal = causal;
+  a.scale_log2 = scale * pdy::kLog2e;
+  const dim3 grid((unsigned)(grid_items(s) * s.hq));
+  if (s.d == 64)
+    hipLaunchKernelGGL(pdy::fwd_kernel<64>, grid, dim3(pdy::FwdCfg<64>::NT),
+                       pdy::FwdCfg<64>::LDS_BYTES, hs, a);
+  else
+    hipLaunchKernelGGL(pdy::fwd_kernel<128>, grid, dim3(pdy::FwdCfg<128>::NT),
+                       pdy::FwdCfg<128>::LDS_BYTES, hs, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "fwd_kernel launch");
+  return PDY_OK;
+}
+
+pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                    const void* dout, const int32_t* cu_seqlens, int32_t num_seqs,
+                    int32_t total_tokens, int32_t max_seqlen, int32_t num_heads_q,
+                    int32_t num_heads_kv, int32_t head_dim, int32_t causal, float scale, float* dq,
+                    float* dk, float* dv, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  Sizes s;
+  pdy_status st;
+  if ((st = check_sizes(total_tokens, num_seqs, max_seqlen, num_heads_q, num_heads_kv, head_dim,
+                        &s)) != PDY_OK)
+    return st;
+  if ((st = check_scale(scale, causal)) != PDY_OK) return st;
+  if (s.T == 0) return PDY_OK;
+  if ((st = check_ptr(q, "q")) || (st = check_ptr(k, "k")) || (st = check_ptr(v, "v")) ||
+      (st = check_ptr(o, "o")) || (st = check_ptr(lse, "lse")) ||
+      (st = check_ptr(dout, "dout")) || (st = check_ptr(dq, "dq")) ||
+      (st = check_ptr(dk, "dk")) || (st = check_ptr(dv, "dv")) ||
+      (st = check_ptr(workspace, "workspace")))
+    return st;
+  if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
+    return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
+  const size_t need = plan_bytes(s) + dd_bytes(s);
+  if (workspace_bytes < need)
+    return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, attn_bwd needs %zu", workspace_bytes,
+                need);
+  hipError_t e = init_kernels();
+  if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  int32_t* ws = reinterpret_cast<int32_t*>(workspace);
+  float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) + plan_bytes(s));
+
+  if ((st = launch_plan(cu_seqlens, ws, s, hs)) != PDY_OK) return st;
+  {
+    const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    if (s.d == 64)
+      hipLaunchKernelGGL(pdy::bwd_pre_kernel<64>, dim3(blocks), dim3(256), 0, hs,
+                         static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
+                         (int)s.T, (int)s.hq);
+    else
+      hipLaunchKernelGGL(pdy::bwd_pre_kernel<128>, dim3(blocks), dim3(256), 0, hs,
+                         static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
+                         (int)s.T, (int)s.hq);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "bwd_pre_kernel launch");
+  }
+  pdy::BwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.lse = lse;
+  a.dd = dd;
+  a.cu = cu_seqlens;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.plan = make_plan(ws, s);
+  a.total_tokens = (int)s.T;
+  a.hq = (int)s.hq;
+  a.hkv = (int)s.hkv;
+  a.causal = causal;
+  a.scale = scale;
+  a.scale_log2 = scale * pdy::kLog2e;
+  const int64_t items = grid_items(s);
+  const dim3 gkv((unsigned)(items * s.hkv));
+  const dim3 gq((unsigned)(items * s.hq));
+  if (s.d == 64) {
+    hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
+                       pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
+    hipLaunchKernelGGL(pdy::bwd_dq_kernel<64>, gq, dim3(pdy::DqCfg<64>::NT),
+                       pdy::DqCfg<64>::LDS_BYTES, hs, a);
+  } else {
+    hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
+                       pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
+    hipLaunchKernelGGL(pdy::bwd_dq_kernel<128>, gq, dim3(pdy::DqCfg<128>::NT),
+                       pdy::DqCfg<128>::LDS_BYTES, hs, a);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
+  return PDY_OK;
+}
+
+pdy_status attn_validate_cu_seqlens(const int32_t* cu_seqlens, int32_t num_seqs,
+                                    int32_t total_tokens, int32_t* max_seqlen_out, void* stream) {
+  g_err[0] = 0;
+  if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (num_seqs < 1) return fail(PDY_ERR_INVALID_ARG, "num_seqs must be >= 1");
+  std::vector<int32_t> h((size_t)num_seqs + 1);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(h.data(), cu_seqlens, h.size() * 4, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "copying cu_seqlens to the host");
+  if (h[0] != 0) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens[0] = %d, expected 0", h[0]);
+  int32_t mx = 0;
+  for (int32_t i = 0; i < num_seqs; ++i) {
+    if (h[i + 1] < h[i])
+      return fail(PDY_ERR_INVALID_ARG, "cu_seqlens decreases at %d (%d -> %d)", i, h[i], h[i + 1]);
+    if (h[i + 1] - h[i] > mx) mx = h[i + 1] - h[i];
+  }
+  if (h[num_seqs] != total_tokens)
+    return fail(PDY_ERR_INVALID_ARG, "cu_seqlens[%d] = %d, expected total_tokens = %d", num_seqs,
+                h[num_seqs], total_tokens);
+  if (max_seqlen_out) *max_seqlen_out = mx;
+  return PDY_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,187 @@
+"""Python binding of the pdyattn C-ABI (include/pdyattn.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of libpdyattn.so.  torch is used for device memory (outputs and the
+workspace are torch allocations) and for the current stream.  There is no
+fallback: if the library is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpdyattn.so")
+
+PDY_OK = 0
+PDY_ERR_INVALID_ARG = -1
+PDY_ERR_UNSUPPORTED = -2
+PDY_ERR_WORKSPACE = -3
+PDY_ERR_HIP = -4
+
+# exported symbols, in the order include/pdyattn.h declares them
+SYMBOLS = ("attn_fwd_workspace_size", "attn_bwd_workspace_size", "attn_fwd", "attn_bwd",
+           "attn_validate_cu_seqlens", "pdy_status_string", "pdy_last_error")
+
+
+class PdyError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: status {status}: {detail}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libpdyattn.so (built in-tree by paper_2511_13198_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2511_13198_amd.build` (no fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    i32, f32, vp, sz = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+    L.attn_fwd_workspace_size.argtypes = [i32] * 6
+    L.attn_fwd_workspace_size.restype = sz
+    L.attn_bwd_workspace_size.argtypes = [i32] * 6
+    L.attn_bwd_workspace_size.restype = sz
+    L.attn_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp, vp, vp, sz, vp]
+    L.attn_fwd.restype = i32
+    L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
+                           vp, vp, vp, vp, sz, vp]
+    L.attn_bwd.restype = i32
+    L.attn_validate_cu_seqlens.argtypes = [vp, i32, i32, ctypes.POINTER(i32), vp]
+    L.attn_validate_cu_seqlens.restype = i32
+    L.pdy_status_string.argtypes = [i32]
+    L.pdy_status_string.restype = ctypes.c_char_p
+    L.pdy_last_error.argtypes = []
+    L.pdy_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str):
+    if status != PDY_OK:
+        L = lib()
+        raise PdyError(status, where,
+                       f"{L.pdy_status_string(status).decode()} ({L.pdy_last_error().decode()})")
+
+
+def last_error() -> str:
+    return lib().pdy_last_error().decode()
+
+
+def _stream_handle(device) -> int:
+    import torch
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def fwd_workspace_size(total_tokens, num_seqs, max_seqlen, hq, hkv, d) -> int:
+    return int(lib().attn_fwd_workspace_size(total_tokens, num_seqs, max_seqlen, hq, hkv, d))
+
+
+def bwd_workspace_size(total_tokens, num_seqs, max_seqlen, hq, hkv, d) -> int:
+    return int(lib().attn_bwd_workspace_size(total_tokens, num_seqs, max_seqlen, hq, hkv, d))
+
+
+def validate_cu_seqlens(cu_seqlens, total_tokens: int) -> int:
+    """Checks cu_seqlens on the host (synchronising) and returns the longest
+    segment length."""
+    out = ctypes.c_int32(0)
+    st = lib().attn_validate_cu_seqlens(cu_seqlens.data_ptr(), cu_seqlens.numel() - 1,
+                                        total_tokens, ctypes.byref(out),
+                                        _stream_handle(cu_seqlens.device))
+    _check(st, "attn_validate_cu_seqlens")
+    return int(out.value)
+
+
+def _check_tensor(t, name, dtype, ndim):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _ws(nbytes: int, device):
+    import torch
+    return torch.empty(max(256, nbytes), dtype=torch.uint8, device=device)
+
+
+def attn_fwd(q, k, v, cu_seqlens, max_seqlen: Optional[int] = None, causal: bool = True,
+             scale: Optional[float] = None, out=None, lse=None, workspace=None):
+    """O [T, Hq, d] bf16 and LSE [Hq, T] fp32 (natural log) of Eq. (2) over
+    the packed batch described by cu_seqlens (int32 [N+1], on the device)."""
+    import torch
+    _check_tensor(q, "q", torch.bfloat16, 3)
+    _check_tensor(k, "k", torch.bfloat16, 3)
+    _check_tensor(v, "v", torch.bfloat16, 3)
+    _check_tensor(cu_seqlens, "cu_seqlens", torch.int32, 1)
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    if tuple(k.shape) != (T, hkv, d) or tuple(v.shape) != (T, hkv, d):
+        raise ValueError("k and v must be [T, Hkv, d] with q's T and d")
+    if max_seqlen is None:
+        max_seqlen = validate_cu_seqlens(cu_seqlens, T)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    n = cu_seqlens.numel() - 1
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((hq, T), dtype=torch.float32, device=q.device)
+    need = fwd_workspace_size(T, n, max_seqlen, hq, hkv, d)
+    if workspace is None:
+        workspace = _ws(need, q.device)
+    st = lib().attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cu_seqlens.data_ptr(), n, T,
+                        int(max_seqlen), hq, hkv, d, int(bool(causal)), float(scale),
+                        out.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
+                        workspace.numel() * workspace.element_size(),
+                        _stream_handle(q.device))
+    _check(st, "attn_fwd")
+    return out, lse
+
+
+def attn_bwd(q, k, v, o, lse, dout, cu_seqlens, max_seqlen: Optional[int] = None,
+             causal: bool = True, scale: Optional[float] = None, dq=None, dk=None, dv=None,
+             workspace=None) -> Tuple:
+    """dQ [T, Hq, d], dK, dV [T, Hkv, d] (fp32) of sum(dout * O)."""
+    import torch
+    for t, name in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
+        _check_tensor(t, name, torch.bfloat16, 3)
+    _check_tensor(lse, "lse", torch.float32, 2)
+    _check_tensor(cu_seqlens, "cu_seqlens", torch.int32, 1)
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    if tuple(o.shape) != (T, hq, d) or tuple(dout.shape) != (T, hq, d):
+        raise ValueError("o and dout must match q")
+    if tuple(lse.shape) != (hq, T):
+        raise ValueError("lse must be [Hq, T]")
+    if max_seqlen is None:
+        max_seqlen = validate_cu_seqlens(cu_seqlens, T)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    n = cu_seqlens.numel() - 1
+    if dq is None:
+        dq = torch.empty((T, hq, d), dtype=torch.float32, device=q.device)
+    if dk is None:
+        dk = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    if dv is None:
+        dv = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    need = bwd_workspace_size(T, n, max_seqlen, hq, hkv, d)
+    if workspace is None:
+        workspace = _ws(need, q.device)
+    st = lib().attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                        dout.data_ptr(), cu_seqlens.data_ptr(), n, T, int(max_seqlen), hq, hkv, d,
+                        int(bool(causal)), float(scale), dq.data_ptr(), dk.data_ptr(),
+                        dv.data_ptr(), workspace.data_ptr(),
+                        workspace.numel() * workspace.element_size(), _stream_handle(q.device))
+    _check(st, "attn_bwd")
+    return dq, dk, dv

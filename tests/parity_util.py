@@ -1,0 +1,142 @@
+"""Helpers shared by the GPU parity tests (HIP path vs the fp64 oracle)."""
+from __future__ import annotations
+
+import math
+import sys
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from paper_2511_13198_amd import workloads as wl
+
+# tolerance for bf16 inputs with fp32 accumulation, applied per tensor
+MAX_ABS = 2e-2
+REL_L2 = 5e-3
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def check_close(name: str, got, ref, max_abs: float = MAX_ABS, rel_l2: float = REL_L2):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, f"{name}: shape {got.shape} vs {ref.shape}"
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values in device output"
+    diff = got - ref
+    mx = float(np.max(np.abs(diff))) if diff.size else 0.0
+    nref = float(np.linalg.norm(ref))
+    rel = float(np.linalg.norm(diff)) / nref if nref > 0 else float(np.linalg.norm(diff))
+    log(f"    {name:5s} max|err| {mx:.3e}  relL2 {rel:.3e}  (n={diff.size})")
+    assert mx <= max_abs, f"{name}: max abs error {mx:.3e} > {max_abs}"
+    assert rel <= rel_l2, f"{name}: relative L2 error {rel:.3e} > {rel_l2}"
+    return mx, rel
+
+
+class HeadView:
+    """[T, H, d] bf16 tensor (host or device) handed to the oracle one head at
+    a time, widened exactly to float64 on the host."""
+
+    def __init__(self, t_bf16):
+        self.t = t_bf16
+        self.num_heads = int(t_bf16.shape[1])
+        self._cache = {}
+
+    def head(self, h: int) -> np.ndarray:
+        if h not in self._cache:
+            if len(self._cache) >= 2:
+                self._cache.pop(next(iter(self._cache)))
+            self._cache[h] = self.t[:, h].contiguous().cpu().double().numpy()
+        return self._cache[h]
+
+
+def to_device_bf16(bits: np.ndarray, device="cuda"):
+    import torch
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def bf16_to_f64(t_bf16) -> np.ndarray:
+    return t_bf16.detach().cpu().double().numpy()
+
+
+def run_gpu(q, k, v, do, cu, max_seqlen, causal, scale, poison=True):
+    """Forward + backward through the C-ABI; outputs poisoned with NaN first so
+    an element the kernels never write is caught."""
+    import torch
+    from paper_2511_13198_amd import pdyattn
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    o = torch.empty_like(q)
+    lse = torch.empty((hq, T), dtype=torch.float32, device=q.device)
+    dq = torch.empty((T, hq, d), dtype=torch.float32, device=q.device)
+    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    if poison:
+        for t in (o, lse, dq, dk, dv):
+            t.fill_(float("nan"))
+    pdyattn.attn_fwd(q, k, v, cu, max_seqlen, causal, scale, out=o, lse=lse)
+    pdyattn.attn_bwd(q, k, v, o, lse, do, cu, max_seqlen, causal, scale, dq=dq, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    return o, lse, dq, dk, dv
+
+
+def sample_rows(lengths: Sequence[int], per_seg_random: int, seed: int = 0,
+                max_rows: Optional[int] = None) -> List[int]:
+    """Stratified query rows: segment edges, tile edges near start/middle/end,
+    and seeded random rows."""
+    rng = np.random.default_rng(seed)
+    rows = set()
+    a = 0
+    for s in lengths:
+        if s == 0:
+            continue
+        b = a + s
+        picks = [0, 1, 2, 3, s - 4, s - 3, s - 2, s - 1]
+        for edge in (64, 128, 256):
+            for c in (edge, s // 2 - s // 2 % edge, s - s % edge):
+                picks += [c - 1, c, c + 1]
+        picks += list(rng.integers(0, s, size=per_seg_random))
+        rows.update(a + int(p) for p in picks if 0 <= p < s)
+        a = b
+    out = sorted(rows)
+    if max_rows is not None and len(out) > max_rows:
+        keep = rng.choice(len(out), size=max_rows, replace=False)
+        out = sorted(out[i] for i in keep)
+    return out
+
+
+def gpu_invariants(o, lse, dq, dk, dv, q, k, v, do, cu_list, scale, causal=True):
+    """Identities of the exact gradient, checked over every element in fp64 on
+    the device (O(T d) work): per segment and key/value head,
+      sum_j dK_j = 0,  sum_j dV_j = sum_i dO_i (over the group),
+      sum_j <V_j, dV_j> = sum_i <dO_i, O_i>,  sum_i <Q_i, dQ_i> = sum_j <K_j, dK_j>.
+    Residuals are relative to the norms of the summed terms."""
+    import torch
+    hq, hkv = q.shape[1], k.shape[1]
+    g = hq // hkv
+    worst = {}
+    for si in range(len(cu_list) - 1):
+        a, b = cu_list[si], cu_list[si + 1]
+        if b - a < 2:
+            continue
+        for hk in range(hkv):
+            hs = slice(hk * g, hk * g + g)
+            dks = dk[a:b, hk].double()
+            dvs = dv[a:b, hk].double()
+            r1 = (dks.sum(0).norm() / (dks.norm() + 1e-30)).item()
+            dos = do[a:b, hs].double()
+            r2 = ((dvs.sum(0) - dos.sum((0, 1))).norm() / (dvs.norm() + 1e-30)).item()
+            lhs = (v[a:b, hk].double() * dvs).sum()
+            rhs = (dos * o[a:b, hs].double()).sum()
+            r3 = (abs(lhs - rhs) / ((v[a:b, hk].double().norm() * dvs.norm()) + 1e-30)).item()
+            lq = (q[a:b, hs].double() * dq[a:b, hs].double()).sum()
+            rk = (k[a:b, hk].double() * dks).sum()
+            r4 = (abs(lq - rk) / ((k[a:b, hk].double().norm() * dks.norm()) + 1e-30)).item()
+            for name, r in (("sum_dK", r1), ("sum_dV", r2), ("V.dV", r3), ("Q.dQ", r4)):
+                worst[name] = max(worst.get(name, 0.0), r)
+    log("    invariants (relative residuals): " +
+        ", ".join(f"{k_}={v_:.2e}" for k_, v_ in worst.items()))
+    for name, r in worst.items():
+        assert r < 5e-3, f"invariant {name} residual {r:.3e}"
+    return worst

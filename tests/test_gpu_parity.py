@@ -1,0 +1,167 @@
+"""HIP path vs the fp64 oracle, through the C-ABI, on seeded inputs.
+
+Small shapes are compared element by element in full; the full-size workloads
+are compared on sampled rows (O, LSE, dQ) and tail key columns (dK, dV) that
+the oracle evaluates one by one, plus identities of the exact gradient over
+every element.  Tolerance per tensor: max |err| <= 2e-2 and relative L2 <= 5e-3."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import attention as ora
+from paper_2511_13198_amd import workloads as wl
+from tests import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+
+def _host_case(lengths, hq, hkv, d, seed=wl.SEED):
+    T = sum(lengths)
+    bits = wl.host_inputs(T, hq, hkv, d, seed=seed)
+    return bits, wl.cu_from_lengths(lengths)
+
+
+def _full_parity(lengths, hq, hkv, d, causal, scale=None, seed=wl.SEED):
+    import torch
+    scale = scale if scale is not None else 1.0 / math.sqrt(d)
+    pu.log(f"  case lengths={lengths[:8]}{'...' if len(lengths) > 8 else ''} T={sum(lengths)} "
+           f"Hq={hq} Hkv={hkv} d={d} causal={causal}")
+    bits, cu = _host_case(lengths, hq, hkv, d, seed)
+    dev = {n: pu.to_device_bf16(b) for n, b in bits.items()}
+    cu_d = torch.from_numpy(cu).cuda()
+    o, lse, dq, dk, dv = pu.run_gpu(dev["q"], dev["k"], dev["v"], dev["do"], cu_d,
+                                    max(lengths) if lengths else 0, causal, scale)
+    f = {n: wl.bf16_bits_to_f64(b) for n, b in bits.items()}
+    ro, rlse, rdq, rdk, rdv = ora.backward(f["q"], f["k"], f["v"], f["do"], cu, causal, scale)
+    pu.check_close("O", pu.bf16_to_f64(o), ro)
+    pu.check_close("LSE", lse.cpu().numpy(), rlse)
+    pu.check_close("dQ", dq.cpu().numpy(), rdq)
+    pu.check_close("dK", dk.cpu().numpy(), rdk)
+    pu.check_close("dV", dv.cpu().numpy(), rdv)
+    return (o, lse, dq, dk, dv), dev, cu_d
+
+
+@pytest.mark.parametrize("lengths,hq,hkv,d,causal,scale", [
+    ([512], 8, 8, 64, True, 0.125),                         # 512-token, 8-head, d=64 workload
+    ([1, 127, 128, 129, 300, 64, 1000], 4, 2, 128, True, None),  # ragged tails + grouped heads
+    ([0, 5, 0, 200, 0], 2, 1, 128, True, None),             # empty segments
+    ([777], 2, 2, 64, False, None),                         # non-causal (BERT-like)
+    ([300, 65, 1], 4, 4, 128, False, None),
+    ([2048, 33], 8, 2, 128, True, None),
+    ([1], 1, 1, 64, True, None),                            # single token
+])
+def test_full_parity_small(lengths, hq, hkv, d, causal, scale):
+    _full_parity(lengths, hq, hkv, d, causal, scale)
+
+
+def test_determinism_and_isolation():
+    """Bitwise: a second run gives the same bytes; a packed batch equals each
+    segment run alone; future keys do not change earlier rows."""
+    import torch
+    lengths = [300, 129, 511]
+    hq, hkv, d = 4, 2, 128
+    bits, cu = _host_case(lengths, hq, hkv, d, seed=3)
+    dev = {n: pu.to_device_bf16(b) for n, b in bits.items()}
+    cu_d = torch.from_numpy(cu).cuda()
+    r1 = pu.run_gpu(dev["q"], dev["k"], dev["v"], dev["do"], cu_d, 511, True, 0.09)
+    r2 = pu.run_gpu(dev["q"], dev["k"], dev["v"], dev["do"], cu_d, 511, True, 0.09)
+    for a, b in zip(r1, r2):
+        assert torch.equal(a, b), "non-deterministic output"
+    for si in range(3):
+        a, b = int(cu[si]), int(cu[si + 1])
+        cu1 = torch.tensor([0, b - a], dtype=torch.int32, device="cuda")
+        alone = pu.run_gpu(*(dev[n][a:b].contiguous() for n in ("q", "k", "v", "do")), cu1,
+                           b - a, True, 0.09)
+        assert torch.equal(alone[0], r1[0][a:b]), f"segment {si}: O differs when packed"
+        assert torch.equal(alone[1], r1[1][:, a:b]), f"segment {si}: LSE differs when packed"
+        for t in (2, 3, 4):
+            assert torch.equal(alone[t], r1[t][a:b]), f"segment {si}: grad {t} differs"
+    # causality: perturb everything after row i of segment 2
+    a = int(cu[2])
+    i = a + 200
+    q2, k2, v2 = (dev[n].clone() for n in ("q", "k", "v"))
+    q2[i + 1:] = 3.0
+    k2[i + 1:] = -2.0
+    v2[i + 1:] = 7.0
+    r3 = pu.run_gpu(q2, k2, v2, dev["do"], cu_d, 511, True, 0.09)
+    assert torch.equal(r3[0][: i + 1], r1[0][: i + 1])
+    assert torch.equal(r3[1][:, : i + 1], r1[1][:, : i + 1])
+    assert torch.equal(r3[2][: i + 1], r1[2][: i + 1])
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads: sampled parity + invariants
+# ---------------------------------------------------------------------------
+def _sampled_parity(w: wl.Workload, device_gen: bool, heads, kv_heads, per_seg_random,
+                    tail_cols, tail_segs=None, max_rows=None):
+    import torch
+    T, hq, hkv, d = w.total_tokens, w.heads_q, w.heads_kv, w.head_dim
+    scale = w.softmax_scale
+    pu.log(f"  workload {w.name}: T={T} N={w.num_seqs} Hq={hq} Hkv={hkv} d={d}")
+    if device_gen:
+        dev = wl.device_inputs(T, hq, hkv, d)
+    else:
+        bits = wl.host_inputs(T, hq, hkv, d)
+        dev = {n: pu.to_device_bf16(b) for n, b in bits.items()}
+    cu = w.cu_seqlens()
+    cu_d = torch.from_numpy(cu).cuda()
+    o, lse, dq, dk, dv = pu.run_gpu(dev["q"], dev["k"], dev["v"], dev["do"], cu_d,
+                                    w.max_seqlen, w.causal, scale)
+    cu_list = [int(x) for x in cu]
+    pu.gpu_invariants(o, lse, dq, dk, dv, dev["q"], dev["k"], dev["v"], dev["do"], cu_list,
+                      scale, w.causal)
+    host = {n: pu.HeadView(t) for n, t in dev.items()}
+    rows = pu.sample_rows(w.lengths, per_seg_random, max_rows=max_rows)
+    res = ora.rows_forward_backward(host["q"], host["k"], host["v"], host["do"], cu, w.causal,
+                                    scale, heads=heads, rows=rows)
+    ridx = torch.tensor(rows, dtype=torch.long, device=o.device)
+    got_o = np.concatenate([o[ridx, h].cpu().double().numpy() for h in heads])
+    got_l = np.concatenate([lse[h, ridx].cpu().double().numpy() for h in heads])
+    got_q = np.concatenate([dq[ridx, h].cpu().double().numpy() for h in heads])
+    pu.check_close("O", got_o, np.concatenate([res[h][0] for h in heads]))
+    pu.check_close("LSE", got_l, np.concatenate([res[h][1] for h in heads]))
+    pu.check_close("dQ", got_q, np.concatenate([res[h][2] for h in heads]))
+    segs = tail_segs if tail_segs is not None else [int(np.argmax(w.lengths))]
+    gk, gv, rk, rv = [], [], [], []
+    for si in segs:
+        b = cu_list[si + 1]
+        lo = max(cu_list[si], b - tail_cols)
+        cols = ora.cols_backward(host["q"], host["k"], host["v"], host["do"], cu, w.causal, scale,
+                                 kv_heads=kv_heads, seg_index=si, col_lo=lo)
+        for hk in kv_heads:
+            gk.append(dk[lo:b, hk].cpu().double().numpy())
+            gv.append(dv[lo:b, hk].cpu().double().numpy())
+            rk.append(cols[hk][0])
+            rv.append(cols[hk][1])
+    pu.check_close("dK", np.concatenate(gk), np.concatenate(rk))
+    pu.check_close("dV", np.concatenate(gv), np.concatenate(rv))
+
+
+def test_packed_65536_loguniform():
+    w = wl.config(2)
+    _sampled_parity(w, device_gen=False, heads=[0, 13, 31], kv_heads=[0, 31],
+                    per_seg_random=8, tail_cols=256, tail_segs=[0, 7, 24])
+
+
+def test_single_131072_h4():
+    _sampled_parity(wl.config(3), device_gen=True, heads=[0, 3], kv_heads=[1, 2],
+                    per_seg_random=96, tail_cols=128)
+
+
+def test_single_638976_h4():
+    _sampled_parity(wl.config(4), device_gen=True, heads=[1, 2], kv_heads=[0, 3],
+                    per_seg_random=48, tail_cols=96, max_rows=96)
+
+
+def test_stream_batches_gqa():
+    stream = wl.stream_config5()
+    # the most-segmented packed batch and the shortest single-sequence batch
+    packed = max(range(len(stream)), key=lambda i: stream[i].num_seqs)
+    single = min((i for i in range(len(stream)) if stream[i].num_seqs == 1),
+                 key=lambda i: stream[i].max_seqlen)
+    for i in (packed, single):
+        w = stream[i]
+        _sampled_parity(w, device_gen=True, heads=[0, 17, 31], kv_heads=[0, 7],
+                        per_seg_random=4 if w.num_seqs > 1 else 32, tail_cols=64,
+                        max_rows=64)
