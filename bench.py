@@ -1,0 +1,190 @@
+#!/usr/bin/env python3
+"""Causal attention forward+backward throughput on one MI355X.
+
+One step = attn_fwd + attn_bwd (every kernel of the hot path) over one packed
+batch whose inputs are already resident in HBM.  Prints ONE JSON line with
+the counted-FLOP throughput (TFLOP/s), the roofline of the dominant kernel
+(timed with HIP events on its own stream inside the library) and the fp64 CPU
+oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+WORKLOADS = {
+    "single131072": 3,   # one 131,072-token sequence, 4 heads (one GPU's head share), d=128
+    "packed65536": 2,    # 65,536 tokens, log-uniform lengths in [128, 8192], 32 heads
+    "single638976": 4,   # one 638,976-token ("624K") sequence, 4 heads
+    "single512": 1,      # 512 tokens, 8 heads, d=64
+}
+
+METRIC = "causal attn fwd+bwd TFLOP/s and % bf16 MFMA peak vs seq length (1 GPU)"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="single131072")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=12288,
+                    help="causal prefix length the CPU oracle is timed on")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, inputs, sample_tokens: int):
+    """Time the fp64 oracle (as it stands) on the causal prefix of head 0:
+    its full forward + backward over the first `sample_tokens` tokens."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import attention as ora
+    from paper_2511_13198_amd import accounting as acc
+    S = min(sample_tokens, w.total_tokens)
+    hk = 0
+    q = inputs["q"][:S, 0:1].cpu().double().numpy()
+    k = inputs["k"][:S, hk:hk + 1].cpu().double().numpy()
+    v = inputs["v"][:S, hk:hk + 1].cpu().double().numpy()
+    do = inputs["do"][:S, 0:1].cpu().double().numpy()
+    cu = np.array([0, S], dtype=np.int64)
+    t0 = time.perf_counter()
+    ora.backward(q, k, v, do, cu, w.causal, w.softmax_scale)
+    dt = time.perf_counter() - t0
+    flops = acc.fwd_bwd_flops([S], 1, w.head_dim, w.causal)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()
+                   if p.get("user_api") == "blas"] or [1])
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"fp64 forward+backward of the causal prefix of the first {S} tokens of "
+                   f"query head 0 of the {w.name} workload ({flops:.3e} counted FLOPs in "
+                   f"{dt:.2f} s; host {platform.processor() or platform.machine()})"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE={world}); multi-GPU runs are not part of this build",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2511_13198_amd import accounting as acc
+    from paper_2511_13198_amd import pdyattn
+    from paper_2511_13198_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    pdyattn.lib()  # fail loudly if the HIP library is missing
+
+    w = wl.config(WORKLOADS[args.workload])
+    T, hq, hkv, d = w.total_tokens, w.heads_q, w.heads_kv, w.head_dim
+    dev = torch.device("cuda:0")
+    inputs = wl.device_inputs(T, hq, hkv, d, device="cuda")
+    q, k, v, do = inputs["q"], inputs["k"], inputs["v"], inputs["do"]
+    cu = torch.from_numpy(w.cu_seqlens()).to(dev)
+    maxlen, scale, causal = w.max_seqlen, w.softmax_scale, w.causal
+    o = torch.empty_like(q)
+    lse = torch.empty((hq, T), dtype=torch.float32, device=dev)
+    dq = torch.empty((T, hq, d), dtype=torch.float32, device=dev)
+    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=dev)
+    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=dev)
+    n = w.num_seqs
+    wsf = torch.empty(max(256, pdyattn.fwd_workspace_size(T, n, maxlen, hq, hkv, d)),
+                      dtype=torch.uint8, device=dev)
+    wsb = torch.empty(max(256, pdyattn.bwd_workspace_size(T, n, maxlen, hq, hkv, d)),
+                      dtype=torch.uint8, device=dev)
+
+    def step():
+        pdyattn.attn_fwd(q, k, v, cu, maxlen, causal, scale, out=o, lse=lse, workspace=wsf)
+        pdyattn.attn_bwd(q, k, v, o, lse, do, cu, maxlen, causal, scale, dq=dq, dk=dk, dv=dv,
+                         workspace=wsb)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] {w.name}: warmup done, timing {args.steps} steps", file=sys.stderr, flush=True)
+    pdyattn.profile_start()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = pdyattn.profile_stop()
+    ms = (t1 - t0) / args.steps * 1e3
+    flops = acc.fwd_bwd_flops(w.lengths, hq, d, causal)
+    value = flops / (ms / 1e3) / 1e12
+
+    kernels_ms = {name: tot / cnt for name, (cnt, tot) in prof.items()}
+    dom = max((kname for kname in kernels_ms if kname in acc.KERNEL_PRODUCTS),
+              key=lambda kname: kernels_ms[kname])
+    dom_flops = acc.kernel_flops(dom, w.lengths, hq, d, causal)
+    achieved = dom_flops / (kernels_ms[dom] / 1e3) / 1e12
+    roofline = {
+        "kernel": dom,
+        "bound": "mfma",
+        "achieved": round(achieved, 2),
+        "peak": acc.PEAK_BF16_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(achieved / acc.PEAK_BF16_TFLOPS, 4),
+        "traffic": None,
+    }
+    print(f"[bench] {ms:.3f} ms/step, {value:.1f} TFLOP/s; kernels (avg ms): "
+          + ", ".join(f"{kk}={vv:.3f}" for kk, vv in kernels_ms.items()),
+          file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, inputs, args.cpu_sample_tokens)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/k/v/dO)",
+        "config": {
+            "workload": w.name,
+            "tokens": T,
+            "segments": n,
+            "max_seqlen": maxlen,
+            "heads_q": hq,
+            "heads_kv": hkv,
+            "head_dim": d,
+            "causal": causal,
+            "counted_flops_per_step": flops,
+        },
+        "pct_of_peak": round(100.0 * value / acc.PEAK_BF16_TFLOPS, 2),
+        "kernels_ms": {kk: round(vv, 4) for kk, vv in kernels_ms.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

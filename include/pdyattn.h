@@ -31,8 +31,8 @@
  *   - Scratch memory comes from the caller's `workspace` (16-byte aligned,
  *     at least the size the matching *_workspace_size query returns).
  *   - Calls on different streams with disjoint outputs and workspaces may run
- *     concurrently; the library holds no global state besides the per-thread
- *     error message.
+ *     concurrently; the library holds no global state besides per-thread
+ *     error text and the optional per-thread kernel timing records.
  *   - Results are bitwise reproducible run to run (no atomics feed outputs).
  */
 #ifndef PDYATTN_H
@@ -103,6 +103,19 @@ const char* pdy_status_string(int32_t status);
 
 /* Detail of the last non-OK status returned on this thread ("" if none). */
 const char* pdy_last_error(void);
+
+/* Kernel timing (measurement support for the per-length cost tables the
+ * paper's hybrid cost models are fitted to, section 4.3).  Between
+ * pdy_profile_start and pdy_profile_stop, every kernel this thread launches
+ * is bracketed by two HIP events recorded on the launch's own stream.
+ * pdy_profile_stop waits for those events and writes, for each kernel id
+ * k < n, the number of launches and their summed duration in milliseconds
+ * (arrays of n caller-owned host elements).  Kernel ids are
+ * 0..pdy_kernel_count()-1, named by pdy_kernel_name. */
+int32_t pdy_kernel_count(void);
+const char* pdy_kernel_name(int32_t k);
+pdy_status pdy_profile_start(void);
+pdy_status pdy_profile_stop(int32_t* launches, double* total_ms, int32_t n);
 
 #ifdef __cplusplus
 }

@@ -73,6 +73,52 @@ pdy_status check_sizes(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// ---------------------------------------------------------------------------
+// Optional per-thread kernel timing: while enabled, every launch is bracketed
+// by two events on its own stream; pdy_profile_stop reduces them per kernel.
+// ---------------------------------------------------------------------------
+enum KernelId { K_PLAN = 0, K_FWD, K_PRE, K_DKDV, K_DQ, K_COUNT };
+const char* const kKernelNames[K_COUNT] = {"plan_kernel", "fwd_kernel", "bwd_pre_kernel",
+                                           "bwd_dkdv_kernel", "bwd_dq_kernel"};
+struct ProfRec {
+  int kid;
+  hipEvent_t a, b;
+};
+thread_local bool g_prof_on = false;
+thread_local std::vector<ProfRec> g_prof_recs;
+thread_local std::vector<hipEvent_t> g_prof_pool;
+
+hipError_t prof_event(hipEvent_t* ev) {
+  if (!g_prof_pool.empty()) {
+    *ev = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(ev);
+}
+
+// Launch through `fn` (which enqueues exactly one kernel on `st`), timing it
+// when profiling is on.  Returns the launch error, if any.
+template <typename F>
+hipError_t launch_timed(int kid, hipStream_t st, F fn) {
+  if (!g_prof_on) {
+    fn();
+    return hipGetLastError();
+  }
+  ProfRec r;
+  r.kid = kid;
+  hipError_t e = prof_event(&r.a);
+  if (e == hipSuccess) e = prof_event(&r.b);
+  if (e == hipSuccess) e = hipEventRecord(r.a, st);
+  if (e != hipSuccess) return e;
+  fn();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(r.b, st);
+  if (e == hipSuccess) g_prof_recs.push_back(r);
+  return e;
+}
+
 size_t plan_bytes(const Sizes& s) { return align256(pdy::plan_ints((int)s.N, s.max_nt) * 4); }
 
 size_t dd_bytes(const Sizes& s) { return align256((size_t)s.hq * (size_t)s.T * 4); }
@@ -128,9 +174,10 @@ pdy_status check_ptr(const void* p, const char* name) {
 }
 
 pdy_status launch_plan(const int32_t* cu, int32_t* ws, const Sizes& s, hipStream_t st) {
-  hipLaunchKernelGGL(pdy::plan_kernel, dim3(1), dim3(pdy::kPlanThreads), 0, st, cu, (int)s.N, kTile,
-                     s.max_nt, ws);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_timed(K_PLAN, st, [&] {
+    hipLaunchKernelGGL(pdy::plan_kernel, dim3(1), dim3(pdy::kPlanThreads), 0, st, cu, (int)s.N,
+                       kTile, s.max_nt, ws);
+  });
   if (e != hipSuccess) return hip_fail(e, "plan_kernel launch");
   return PDY_OK;
 }
@@ -209,13 +256,14 @@ pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* 
   a.causal = causal;
   a.scale_log2 = scale * pdy::kLog2e;
   const dim3 grid((unsigned)(grid_items(s) * s.hq));
-  if (s.d == 64)
-    hipLaunchKernelGGL(pdy::fwd_kernel<64>, grid, dim3(pdy::FwdCfg<64>::NT),
-                       pdy::FwdCfg<64>::LDS_BYTES, hs, a);
-  else
-    hipLaunchKernelGGL(pdy::fwd_kernel<128>, grid, dim3(pdy::FwdCfg<128>::NT),
-                       pdy::FwdCfg<128>::LDS_BYTES, hs, a);
-  e = hipGetLastError();
+  e = launch_timed(K_FWD, hs, [&] {
+    if (s.d == 64)
+      hipLaunchKernelGGL(pdy::fwd_kernel<64>, grid, dim3(pdy::FwdCfg<64>::NT),
+                         pdy::FwdCfg<64>::LDS_BYTES, hs, a);
+    else
+      hipLaunchKernelGGL(pdy::fwd_kernel<128>, grid, dim3(pdy::FwdCfg<128>::NT),
+                         pdy::FwdCfg<128>::LDS_BYTES, hs, a);
+  });
   if (e != hipSuccess) return hip_fail(e, "fwd_kernel launch");
   return PDY_OK;
 }
@@ -256,15 +304,16 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   {
     const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
     const unsigned blocks = (unsigned)((threads + 255) / 256);
-    if (s.d == 64)
-      hipLaunchKernelGGL(pdy::bwd_pre_kernel<64>, dim3(blocks), dim3(256), 0, hs,
-                         static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
-                         (int)s.T, (int)s.hq);
-    else
-      hipLaunchKernelGGL(pdy::bwd_pre_kernel<128>, dim3(blocks), dim3(256), 0, hs,
-                         static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
-                         (int)s.T, (int)s.hq);
-    e = hipGetLastError();
+    e = launch_timed(K_PRE, hs, [&] {
+      if (s.d == 64)
+        hipLaunchKernelGGL(pdy::bwd_pre_kernel<64>, dim3(blocks), dim3(256), 0, hs,
+                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
+                           (int)s.T, (int)s.hq);
+      else
+        hipLaunchKernelGGL(pdy::bwd_pre_kernel<128>, dim3(blocks), dim3(256), 0, hs,
+                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
+                           (int)s.T, (int)s.hq);
+    });
     if (e != hipSuccess) return hip_fail(e, "bwd_pre_kernel launch");
   }
   pdy::BwdArgs a;
@@ -288,19 +337,24 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   const int64_t items = grid_items(s);
   const dim3 gkv((unsigned)(items * s.hkv));
   const dim3 gq((unsigned)(items * s.hq));
-  if (s.d == 64) {
-    hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
-                       pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
-    hipLaunchKernelGGL(pdy::bwd_dq_kernel<64>, gq, dim3(pdy::DqCfg<64>::NT),
-                       pdy::DqCfg<64>::LDS_BYTES, hs, a);
-  } else {
-    hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
-                       pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
-    hipLaunchKernelGGL(pdy::bwd_dq_kernel<128>, gq, dim3(pdy::DqCfg<128>::NT),
-                       pdy::DqCfg<128>::LDS_BYTES, hs, a);
-  }
-  e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
+  e = launch_timed(K_DKDV, hs, [&] {
+    if (s.d == 64)
+      hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
+                         pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
+    else
+      hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
+                         pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
+  });
+  if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
+  e = launch_timed(K_DQ, hs, [&] {
+    if (s.d == 64)
+      hipLaunchKernelGGL(pdy::bwd_dq_kernel<64>, gq, dim3(pdy::DqCfg<64>::NT),
+                         pdy::DqCfg<64>::LDS_BYTES, hs, a);
+    else
+      hipLaunchKernelGGL(pdy::bwd_dq_kernel<128>, gq, dim3(pdy::DqCfg<128>::NT),
+                         pdy::DqCfg<128>::LDS_BYTES, hs, a);
+  });
+  if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
   return PDY_OK;
 }
 
@@ -326,6 +380,49 @@ pdy_status attn_validate_cu_seqlens(const int32_t* cu_seqlens, int32_t num_seqs,
                 h[num_seqs], total_tokens);
   if (max_seqlen_out) *max_seqlen_out = mx;
   return PDY_OK;
+}
+
+int32_t pdy_kernel_count(void) { return K_COUNT; }
+
+const char* pdy_kernel_name(int32_t k) {
+  return (k >= 0 && k < K_COUNT) ? kKernelNames[k] : "";
+}
+
+pdy_status pdy_profile_start(void) {
+  g_err[0] = 0;
+  for (auto& r : g_prof_recs) {
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+  }
+  g_prof_recs.clear();
+  g_prof_on = true;
+  return PDY_OK;
+}
+
+pdy_status pdy_profile_stop(int32_t* launches, double* total_ms, int32_t n) {
+  g_err[0] = 0;
+  g_prof_on = false;
+  if (n < 0 || (n > 0 && (launches == nullptr || total_ms == nullptr)))
+    return fail(PDY_ERR_INVALID_ARG, "pdy_profile_stop: bad output arrays");
+  for (int32_t k = 0; k < n; ++k) {
+    launches[k] = 0;
+    total_ms[k] = 0.0;
+  }
+  pdy_status st = PDY_OK;
+  for (auto& r : g_prof_recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess && st == PDY_OK) st = hip_fail(e, "pdy_profile_stop: reading events");
+    if (r.kid < n) {
+      launches[r.kid] += 1;
+      total_ms[r.kid] += ms;
+    }
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+  }
+  g_prof_recs.clear();
+  return st;
 }
 
 }  // extern "C"

@@ -23,7 +23,8 @@ PDY_ERR_HIP = -4
 
 # exported symbols, in the order include/pdyattn.h declares them
 SYMBOLS = ("attn_fwd_workspace_size", "attn_bwd_workspace_size", "attn_fwd", "attn_bwd",
-           "attn_validate_cu_seqlens", "pdy_status_string", "pdy_last_error")
+           "attn_validate_cu_seqlens", "pdy_status_string", "pdy_last_error",
+           "pdy_kernel_count", "pdy_kernel_name", "pdy_profile_start", "pdy_profile_stop")
 
 
 class PdyError(RuntimeError):
@@ -60,6 +61,14 @@ def lib() -> ctypes.CDLL:
     L.pdy_status_string.restype = ctypes.c_char_p
     L.pdy_last_error.argtypes = []
     L.pdy_last_error.restype = ctypes.c_char_p
+    L.pdy_kernel_count.argtypes = []
+    L.pdy_kernel_count.restype = i32
+    L.pdy_kernel_name.argtypes = [i32]
+    L.pdy_kernel_name.restype = ctypes.c_char_p
+    L.pdy_profile_start.argtypes = []
+    L.pdy_profile_start.restype = i32
+    L.pdy_profile_stop.argtypes = [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double), i32]
+    L.pdy_profile_stop.restype = i32
     _lib = L
     return L
 
@@ -69,6 +78,23 @@ def _check(status: int, where: str):
         L = lib()
         raise PdyError(status, where,
                        f"{L.pdy_status_string(status).decode()} ({L.pdy_last_error().decode()})")
+
+
+def profile_start():
+    """Start bracketing every kernel this thread launches with HIP events."""
+    _check(lib().pdy_profile_start(), "pdy_profile_start")
+
+
+def profile_stop() -> dict:
+    """Stop timing; returns {kernel name: (launches, total ms)} for kernels
+    launched since profile_start (waits for their events)."""
+    L = lib()
+    n = L.pdy_kernel_count()
+    launches = (ctypes.c_int32 * n)()
+    total = (ctypes.c_double * n)()
+    _check(L.pdy_profile_stop(launches, total, n), "pdy_profile_stop")
+    return {L.pdy_kernel_name(i).decode(): (int(launches[i]), float(total[i]))
+            for i in range(n) if launches[i] > 0}
 
 
 def last_error() -> str:
