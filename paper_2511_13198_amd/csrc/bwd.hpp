@@ -16,6 +16,7 @@
 // All outputs are deterministic.
 #pragma once
 #include "common.hpp"
+#include "fwd.hpp"  // acc_row_off
 
 namespace pdy {
 
@@ -60,7 +61,8 @@ struct BwdArgs {
   float* dq;
   float* dk;
   float* dv;
-  Plan plan;
+  Plan plan;    // tiles of DkdvCfg::BK keys
+  Plan plan_q;  // tiles of DqCfg::BQ query rows
   int total_tokens;
   int hq;
   int hkv;
@@ -75,8 +77,7 @@ struct DkdvCfg {
   static constexpr int BQ = 64;   // query rows per step
   static constexpr int NW = 4;
   static constexpr int NT = NW * 64;
-  static constexpr int PITCH = D + 8;
-  static constexpr int TILE = BQ * PITCH;
+  static constexpr int TILE = BQ * LdsTile<D>::ROW;
   // per stage: Q tile, dO tile, lse2[BQ], D[BQ]
   static constexpr int STAGE = 2 * TILE * 2 + 2 * BQ * 4;
   static constexpr int LDS_BYTES = 2 * STAGE;
@@ -85,7 +86,7 @@ struct DkdvCfg {
 template <int D>
 __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
   using C = DkdvCfg<D>;
-  constexpr int BK = C::BK, BQ = C::BQ, PITCH = C::PITCH;
+  constexpr int BK = C::BK, BQ = C::BQ;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   const int item = blockIdx.x / a.hkv;
@@ -151,8 +152,8 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
   };
   auto commit = [&](int buf) {
     uint8_t* st = stage_ptr(buf);
-    ql.store(reinterpret_cast<uint16_t*>(st), PITCH);
-    gl.store(reinterpret_cast<uint16_t*>(st) + C::TILE, PITCH);
+    ql.store(reinterpret_cast<uint16_t*>(st));
+    gl.store(reinterpret_cast<uint16_t*>(st) + C::TILE);
     float* stats = reinterpret_cast<float*>(st + 2 * C::TILE * 2);
     if (threadIdx.x < BQ) {
       stats[threadIdx.x] = lse_r;
@@ -186,8 +187,8 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
         f32x16 dp = zero16();
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(lds_row_operand(qs, PITCH, rb * 32, ks * 16), kf[ks], s);
-          dp = mfma32(lds_row_operand(gs, PITCH, rb * 32, ks * 16), vf[ks], dp);
+          s = mfma32(lds_row_operand<D>(qs, rb * 32, ks * 16), kf[ks], s);
+          dp = mfma32(lds_row_operand<D>(gs, rb * 32, ks * 16), vf[ks], dp);
         }
 #pragma unroll
         for (int grp = 0; grp < 4; ++grp) {
@@ -215,8 +216,8 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
         bf16x8 sb = pack8(ds[t >> 1], (t & 1) * 8);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          dva[db] = mfma32(lds_tr_a_operand(gs, PITCH, t * 16, db * 32), pb, dva[db]);
-          dka[db] = mfma32(lds_tr_a_operand(qs, PITCH, t * 16, db * 32), sb, dka[db]);
+          dva[db] = mfma32(lds_tr_a_operand<D>(gs, t * 16, db * 32), pb, dva[db]);
+          dka[db] = mfma32(lds_tr_a_operand<D>(qs, t * 16, db * 32), sb, dka[db]);
         }
       }
     }
@@ -241,27 +242,25 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
   }
 }
 
-template <int D>
+template <int D, int NW>
 struct DqCfg {
-  static constexpr int BQ = 128;
+  static constexpr int BQ = 32 * NW;
   static constexpr int BK = 64;
-  static constexpr int NW = 4;
   static constexpr int NT = NW * 64;
-  static constexpr int PITCH = D + 8;
-  static constexpr int TILE = BK * PITCH;
+  static constexpr int TILE = BK * LdsTile<D>::ROW;
   static constexpr int LDS_BYTES = 2 * 2 * TILE * 2;
 };
 
-template <int D>
-__global__ void __launch_bounds__(256, 1) bwd_dq_kernel(BwdArgs a) {
-  using C = DqCfg<D>;
-  constexpr int BQ = C::BQ, BK = C::BK, PITCH = C::PITCH;
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) bwd_dq_kernel(BwdArgs a) {
+  using C = DqCfg<D, NW>;
+  constexpr int BQ = C::BQ, BK = C::BK;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   const int item = blockIdx.x / a.hq;
   const int h = blockIdx.x % a.hq;
   int seg, level;
-  if (!plan_lookup(a.plan, item, seg, level)) return;
+  if (!plan_lookup(a.plan_q, item, seg, level)) return;
   const int seg_lo = a.cu[seg];
   const int seg_hi = a.cu[seg + 1];
   const int q0 = seg_lo + level * BQ;
@@ -273,6 +272,7 @@ __global__ void __launch_bounds__(256, 1) bwd_dq_kernel(BwdArgs a) {
   const int row = q0 + w * 32 + (l & 31);
   const int wrow0 = q0 + w * 32;
   const int wrow_last = wrow0 + 31;
+  const int key_lim = a.causal ? min(row, seg_hi - 1) : seg_hi - 1;
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
 
@@ -304,19 +304,18 @@ __global__ void __launch_bounds__(256, 1) bwd_dq_kernel(BwdArgs a) {
   TileLoader<BK, D, C::NT> kl, vl;
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  if (ntiles > 0) {
-    kl.load(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-    vl.load(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-    kl.store(kbuf(0), PITCH);
-    vl.store(vbuf(0), PITCH);
-  }
+  // rows past the segment end repeat the last key; they are always masked
+  kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+  vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+  kl.store(kbuf(0));
+  vl.store(vbuf(0));
   for (int it = 0; it < ntiles; ++it) {
     const int k0 = seg_lo + it * BK;
     const bool more = it + 1 < ntiles;
     if (more) {
       const int k1 = k0 + BK;
-      kl.load(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-      vl.load(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
     }
     __syncthreads();
     const uint16_t* ks_ = kbuf(it & 1);
@@ -324,38 +323,34 @@ __global__ void __launch_bounds__(256, 1) bwd_dq_kernel(BwdArgs a) {
     const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
     if (active) {
       const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
-      f32x16 ds[BK / 32];
+      // one 32-key block at a time keeps S^T and dP^T to 32 registers
 #pragma unroll
       for (int kb = 0; kb < BK / 32; ++kb) {
-        f32x16 s = zero16();
-        f32x16 dp = zero16();
+        f32x16 s = zero16(), dp = zero16();
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(lds_row_operand(ks_, PITCH, kb * 32, ks * 16), qf[ks], s);
-          dp = mfma32(lds_row_operand(vs_, PITCH, kb * 32, ks * 16), gf[ks], dp);
+          s = mfma32(lds_row_operand<D>(ks_, kb * 32, ks * 16), qf[ks], s);
+          dp = mfma32(lds_row_operand<D>(vs_, kb * 32, ks * 16), gf[ks], dp);
         }
+        const int lim = key_lim - (k0 + kb * 32 + hh * 4);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -lse2));
-          if (need_mask) {
-            const int key = k0 + kb * 32 + (r >> 2) * 8 + hh * 4 + (r & 3);
-            const bool vis = key < seg_hi && (!a.causal || key <= row);
-            if (!vis) pv = 0.f;
-          }
-          ds[kb][r] = pv * (dp[r] - ddv);
+          if (need_mask && acc_row_off(r) > lim) pv = 0.f;
+          s[r] = pv * (dp[r] - ddv);  // dS^T
         }
-      }
 #pragma unroll
-      for (int t = 0; t < BK / 16; ++t) {
-        bf16x8 sb = pack8(ds[t >> 1], (t & 1) * 8);
+        for (int t2 = 0; t2 < 2; ++t2) {
+          const bf16x8 sb = pack8(s, t2 * 8);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-          dqa[db] = mfma32(lds_tr_a_operand(ks_, PITCH, t * 16, db * 32), sb, dqa[db]);
+          for (int db = 0; db < D / 32; ++db)
+            dqa[db] = mfma32(lds_tr_a_operand<D>(ks_, kb * 32 + t2 * 16, db * 32), sb, dqa[db]);
+        }
       }
     }
     if (more) {
-      kl.store(kbuf((it + 1) & 1), PITCH);
-      vl.store(vbuf((it + 1) & 1), PITCH);
+      kl.store(kbuf((it + 1) & 1));
+      vl.store(vbuf((it + 1) & 1));
     }
   }
 

@@ -73,12 +73,34 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p, bool valid) {
   return __builtin_bit_cast(bf16x8, raw);
 }
 
+// ---------------------------------------------------------------------------
+// LDS tile layout.  A tile holds rows of D bf16 values as 16-byte chunks.
+// For D = 128 a row is exactly 256 bytes (all 64 banks) and chunk c of row r
+// is stored at chunk position c ^ swz(r), swz(r) = 4*(r % 4) + (r / 4) % 4.
+// That makes both access patterns below conflict-free:
+//   * row reads (16 lanes = 16 consecutive rows, one chunk each): swz is a
+//     bijection on any 16 consecutive rows aligned to 16;
+//   * transposing reads (32 lanes = 4 consecutive rows x 4 consecutive
+//     chunks, rows and chunks aligned to 4): the low two bits of the
+//     position come from the chunk, the high two from the row.
+// For D = 64 rows are padded to 72 elements instead.
+// ---------------------------------------------------------------------------
+template <int D>
+struct LdsTile {
+  static constexpr int ROW = (D == 128) ? 128 : D + 8;  // elements per stored row
+  __device__ __forceinline__ static int off(int r, int chunk) {
+    if constexpr (D == 128) return r * 128 + ((chunk ^ ((r & 3) * 4 + ((r >> 2) & 3))) << 3);
+    else return r * ROW + (chunk << 3);
+  }
+  static constexpr int bytes(int rows) { return rows * ROW * 2; }
+};
+
 // A/B operand whose 8 contraction elements are contiguous in an LDS row:
 // element j of lane l comes from row (row0 + l % 32), column (col0 + (l/32)*8 + j).
-__device__ __forceinline__ bf16x8 lds_row_operand(const uint16_t* tile, int pitch, int row0,
-                                                  int col0) {
+template <int D>
+__device__ __forceinline__ bf16x8 lds_row_operand(const uint16_t* tile, int row0, int col0) {
   const int l = __lane_id();
-  const uint16_t* p = tile + (row0 + (l & 31)) * pitch + col0 + (l >> 5) * 8;
+  const uint16_t* p = tile + LdsTile<D>::off(row0 + (l & 31), (col0 >> 3) + (l >> 5));
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
 }
 
@@ -88,16 +110,18 @@ __device__ __forceinline__ bf16x8 lds_row_operand(const uint16_t* tile, int pitc
 // group of 16 lanes, lane i addresses row (base + i/4), 4 columns starting at
 // col0 + (group % 2) * 16 + 4 * (i % 4); the instruction hands lane i the
 // element (i % 4) of the rows addressed by lanes 4e + i/4, e = 0..3.
-__device__ __forceinline__ bf16x8 lds_tr_a_operand(const uint16_t* tile, int pitch, int row0,
-                                                   int col0) {
+// row0 must be a multiple of 16 and col0 a multiple of 32.
+template <int D>
+__device__ __forceinline__ bf16x8 lds_tr_a_operand(const uint16_t* tile, int row0, int col0) {
   const int l = __lane_id();
   const int hh = l >> 5;
   const int g2 = (l >> 4) & 1;
   const int i = l & 15;
   const int row = row0 + hh * 4 + (i >> 2);
-  const int col = col0 + g2 * 16 + 4 * (i & 3);
-  const uint16_t* p0 = tile + row * pitch + col;
-  const uint16_t* p1 = p0 + 8 * pitch;
+  const int chunk = (col0 >> 3) + g2 * 2 + ((i & 3) >> 1);
+  const int sub = (i & 1) * 4;
+  const uint16_t* p0 = tile + LdsTile<D>::off(row, chunk) + sub;
+  const uint16_t* p1 = tile + LdsTile<D>::off(row + 8, chunk) + sub;
   i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
   i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
   bf16x4 blo = __builtin_bit_cast(bf16x4, lo);
@@ -112,8 +136,8 @@ __device__ __forceinline__ bf16x8 lds_tr_a_operand(const uint16_t* tile, int pit
 }
 
 // Cooperative copy of a [rows x D] bf16 tile (rows of global stride
-// `gstride` elements) into registers: NT threads, 16 B per thread per step.
-// Rows >= valid_rows read as zero.
+// `gstride` elements) into registers: NT threads, 16 B per thread per step,
+// then into an LdsTile<D> layout.
 template <int ROWS, int D, int NT>
 struct TileLoader {
   static constexpr int CHUNKS_PER_ROW = D / 8;
@@ -122,6 +146,7 @@ struct TileLoader {
   static_assert(TOTAL % NT == 0, "tile must split evenly over the workgroup");
   u32x4 regs[STEPS];
 
+  // Rows >= valid_rows read as zero.
   __device__ __forceinline__ void load(const uint16_t* base, size_t gstride, int valid_rows) {
     const int t = threadIdx.x;
 #pragma unroll
@@ -134,14 +159,29 @@ struct TileLoader {
       regs[s] = v;
     }
   }
-  __device__ __forceinline__ void store(uint16_t* lds, int pitch) const {
+  // Rows >= valid_rows (valid_rows >= 1) repeat the last valid row instead of
+  // reading zeros: no branch per chunk.  Only for tiles whose out-of-range
+  // rows the caller masks out (their probabilities are exactly zero).
+  __device__ __forceinline__ void load_clamped(const uint16_t* base, size_t gstride,
+                                               int valid_rows) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      const int c = t + s * NT;
+      int row = c / CHUNKS_PER_ROW;
+      row = row < valid_rows ? row : valid_rows - 1;
+      const int col = (c % CHUNKS_PER_ROW) * 8;
+      regs[s] = *reinterpret_cast<const u32x4*>(base + (size_t)row * gstride + col);
+    }
+  }
+  __device__ __forceinline__ void store(uint16_t* lds) const {
     const int t = threadIdx.x;
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
       const int c = t + s * NT;
       const int row = c / CHUNKS_PER_ROW;
-      const int col = (c % CHUNKS_PER_ROW) * 8;
-      *reinterpret_cast<u32x4*>(lds + row * pitch + col) = regs[s];
+      const int chunk = c % CHUNKS_PER_ROW;
+      *reinterpret_cast<u32x4*>(lds + LdsTile<D>::off(row, chunk)) = regs[s];
     }
   }
 };

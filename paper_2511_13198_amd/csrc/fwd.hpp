@@ -1,8 +1,10 @@
 // Forward of Eq. (2) (section 3): tiled online-softmax attention on the bf16
 // matrix cores of gfx950.
 //
-// One workgroup = one (segment, query head, query tile of 128 rows); each of
-// its 4 waves owns 32 query rows, with Q held in registers as the B operand of
+// One workgroup = one (segment, query head, query tile of 32*NW rows).  With
+// NW = 8 two waves share each SIMD, so one wave's softmax (VALU) overlaps the
+// other's matrix products.  Each wave owns 32 query rows, with Q held in
+// registers as the B operand of
 //   S^T = K Q^T            (32 keys x 32 rows per MFMA tile, keys from LDS)
 // so that each lane owns one query row (l % 32) and half of the keys of a
 // tile; the row max / row sum need one cross-half exchange (permlane32_swap).
@@ -12,21 +14,26 @@
 // 64 keys are double-buffered: the global loads of tile t+1 are in flight while
 // tile t is computed.  Tiles entirely above the causal diagonal are never
 // visited; only tiles crossing the diagonal or the segment end are masked.
-// The row statistics are kept in base 2 (log2(e) is folded into the scale) and
-// converted back for the natural-log LSE output.
+//
+// Softmax statistics are kept in base 2 (log2(e) folded into the scale).  The
+// running max used as the exponent offset is only raised when a new tile's max
+// exceeds it by more than kRescaleSlack (then the accumulators are rescaled);
+// otherwise probabilities up to 2^kRescaleSlack are accumulated as they are.
+// The final O = acc / l and LSE = m + log2(l) use the same offset, so the
+// result is the same as with exact rescaling at every tile.
 #pragma once
 #include "common.hpp"
 
 namespace pdy {
 
-template <int D>
+constexpr float kRescaleSlack = 8.0f;
+
+template <int D, int NW>
 struct FwdCfg {
-  static constexpr int BQ = 128;
+  static constexpr int BQ = 32 * NW;
   static constexpr int BK = 64;
-  static constexpr int NW = 4;
   static constexpr int NT = NW * 64;
-  static constexpr int PITCH = D + 8;  // LDS row pitch in bf16 elements
-  static constexpr int TILE = BK * PITCH;
+  static constexpr int TILE = BK * LdsTile<D>::ROW;  // elements per LDS tile
   static constexpr int LDS_BYTES = 2 * 2 * TILE * 2;  // {K, V} x double buffer
 };
 
@@ -45,10 +52,13 @@ struct FwdArgs {
   float scale_log2;  // scale * log2(e)
 };
 
-template <int D>
-__global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
-  using C = FwdCfg<D>;
-  constexpr int BQ = C::BQ, BK = C::BK, PITCH = C::PITCH;
+// key offset within a 32-key block held in accumulator register r (lane half 0)
+__device__ __forceinline__ constexpr int acc_row_off(int r) { return (r >> 2) * 8 + (r & 3); }
+
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
+  using C = FwdCfg<D, NW>;
+  constexpr int BQ = C::BQ, BK = C::BK;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   const int item = blockIdx.x / a.hq;
@@ -66,6 +76,8 @@ __global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
   const int row = q0 + w * 32 + (l & 31);  // this lane's query row
   const int wrow0 = q0 + w * 32;
   const int wrow_last = wrow0 + 31;
+  // last key this row may see
+  const int key_lim = a.causal ? min(row, seg_hi - 1) : seg_hi - 1;
 
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
@@ -82,7 +94,7 @@ __global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) oacc[i] = zero16();
-  float m = -INFINITY;  // running max of scaled logits (base 2)
+  float m = -INFINITY;  // exponent offset (base-2 scaled logits)
   float lsum = 0.f;     // partial row sum over this lane's keys
 
   const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
@@ -95,21 +107,19 @@ __global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
   TileLoader<BK, D, C::NT> kl, vl;
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  {
-    const int k0 = seg_lo;
-    kl.load(kbase + (size_t)k0 * kvstride, kvstride, seg_hi - k0);
-    vl.load(vbase + (size_t)k0 * kvstride, kvstride, seg_hi - k0);
-    kl.store(kbuf(0), PITCH);
-    vl.store(vbuf(0), PITCH);
-  }
+  // rows past the segment end repeat the last key; they are always masked
+  kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+  vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+  kl.store(kbuf(0));
+  vl.store(vbuf(0));
 
   for (int it = 0; it < ntiles; ++it) {
     const int k0 = seg_lo + it * BK;
     const bool more = it + 1 < ntiles;
     if (more) {
       const int k1 = k0 + BK;
-      kl.load(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-      vl.load(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
     }
     __syncthreads();
     const uint16_t* ks_ = kbuf(it & 1);
@@ -117,27 +127,25 @@ __global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
 
     const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
     if (active) {
-      // S^T for two 32-key blocks
+      // S^T for the tile's 32-key blocks; the independent chains interleave
       f32x16 s[BK / 32];
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) {
-        s[kb] = zero16();
+      for (int kb = 0; kb < BK / 32; ++kb) s[kb] = zero16();
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          bf16x8 kf = lds_row_operand(ks_, PITCH, kb * 32, ks * 16);
-          s[kb] = mfma32(kf, qf[ks], s[kb]);
-        }
-      }
+      for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+        for (int kb = 0; kb < BK / 32; ++kb)
+          s[kb] = mfma32(lds_row_operand<D>(ks_, kb * 32, ks * 16), qf[ks], s[kb]);
+
       const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
       if (need_mask) {
 #pragma unroll
-        for (int kb = 0; kb < BK / 32; ++kb)
+        for (int kb = 0; kb < BK / 32; ++kb) {
+          const int lim = key_lim - (k0 + kb * 32 + hh * 4);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = k0 + kb * 32 + (r >> 2) * 8 + hh * 4 + (r & 3);
-            const bool vis = key < seg_hi && (!a.causal || key <= row);
-            if (!vis) s[kb][r] = -INFINITY;
-          }
+          for (int r = 0; r < 16; ++r)
+            if (acc_row_off(r) > lim) s[kb][r] = -INFINITY;
+        }
       }
       float tmax = -INFINITY;
 #pragma unroll
@@ -145,10 +153,18 @@ __global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
       tmax = fmaxf(tmax, partner32(tmax));
-      const float mnew = fmaxf(m, tmax * a.scale_log2);
-      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
-      const float alpha = fast_exp2(m - muse);
-      m = mnew;
+      const float mt = tmax * a.scale_log2;
+      const bool grow = mt > m + kRescaleSlack;
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+        const float alpha = grow ? fast_exp2(m - mt) : 1.f;
+        m = grow ? mt : m;
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      }
+      const float muse = (m == -INFINITY) ? 0.f : m;
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < BK / 32; ++kb)
@@ -158,25 +174,19 @@ __global__ void __launch_bounds__(256, 1) fwd_kernel(FwdArgs a) {
           s[kb][r] = p;
           psum += p;
         }
-      lsum = lsum * alpha + psum;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      // O^T += V^T P^T over 4 key steps of 16
+      lsum += psum;
+      // O^T += V^T P^T over the tile's 16-key steps
 #pragma unroll
       for (int t = 0; t < BK / 16; ++t) {
-        bf16x8 pf = pack8(s[t >> 1], (t & 1) * 8);
+        const bf16x8 pf = pack8(s[t >> 1], (t & 1) * 8);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          bf16x8 vf = lds_tr_a_operand(vs_, PITCH, t * 16, db * 32);
-          oacc[db] = mfma32(vf, pf, oacc[db]);
-        }
+        for (int db = 0; db < D / 32; ++db)
+          oacc[db] = mfma32(lds_tr_a_operand<D>(vs_, t * 16, db * 32), pf, oacc[db]);
       }
     }
     if (more) {
-      kl.store(kbuf((it + 1) & 1), PITCH);
-      vl.store(vbuf((it + 1) & 1), PITCH);
+      kl.store(kbuf((it + 1) & 1));
+      vl.store(vbuf((it + 1) & 1));
     }
   }
 

@@ -30,14 +30,22 @@ pdy_status hip_fail(hipError_t e, const char* what) {
   return fail(PDY_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr int kTile = 128;  // schedule granularity shared by every kernel
+constexpr int kTile = 128;  // schedule granularity of the backward kernels
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 struct Sizes {
   int64_t T, N, maxlen, hq, hkv, d;
-  int max_nt;
+  int max_nt;  // tiles of kTile in the longest segment
 };
+
+int tiles_of(const Sizes& s, int tile) {
+  const int64_t n = (s.maxlen + tile - 1) / tile;
+  return n < 1 ? 1 : (int)n;
+}
+
+// forward workgroup size: 8 waves (256 query rows) unless segments are short
+int fwd_waves(const Sizes& s) { return s.maxlen > 128 ? 8 : 4; }
 
 pdy_status check_sizes(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv, int32_t d,
                        Sizes* out) {
@@ -119,22 +127,26 @@ hipError_t launch_timed(int kid, hipStream_t st, F fn) {
   return e;
 }
 
-size_t plan_bytes(const Sizes& s) { return align256(pdy::plan_ints((int)s.N, s.max_nt) * 4); }
+size_t plan_bytes(const Sizes& s, int tile) {
+  return align256(pdy::plan_ints((int)s.N, tiles_of(s, tile)) * 4);
+}
 
 size_t dd_bytes(const Sizes& s) { return align256((size_t)s.hq * (size_t)s.T * 4); }
 
-pdy::Plan make_plan(int32_t* ws, const Sizes& s) {
+pdy::Plan make_plan(int32_t* ws, const Sizes& s, int tile) {
+  const int nt = tiles_of(s, tile);
   pdy::Plan p;
   p.order = ws + s.N;
-  p.start = ws + 2 * s.N + s.max_nt;
-  p.total = ws + 2 * s.N + 2 * s.max_nt;
-  p.max_nt = s.max_nt;
+  p.start = ws + 2 * s.N + nt;
+  p.total = ws + 2 * s.N + 2 * nt;
+  p.max_nt = nt;
   return p;
 }
 
-int64_t grid_items(const Sizes& s) {
-  const int64_t bound1 = s.T / kTile + s.N;
-  const int64_t bound2 = s.N * (int64_t)s.max_nt;
+// upper bound on sum_i ceil(len_i / tile) (the number of work items)
+int64_t grid_items(const Sizes& s, int tile) {
+  const int64_t bound1 = s.T / tile + s.N;
+  const int64_t bound2 = s.N * (int64_t)tiles_of(s, tile);
   return bound1 < bound2 ? bound1 : bound2;
 }
 
@@ -148,16 +160,38 @@ hipError_t set_lds(K kernel, int bytes) {
 hipError_t init_kernels() {
   static hipError_t status = [] {
     hipError_t e;
-    if ((e = set_lds(pdy::fwd_kernel<64>, pdy::FwdCfg<64>::LDS_BYTES)) != hipSuccess) return e;
-    if ((e = set_lds(pdy::fwd_kernel<128>, pdy::FwdCfg<128>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::fwd_kernel<64, 4>, pdy::FwdCfg<64, 4>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::fwd_kernel<64, 8>, pdy::FwdCfg<64, 8>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::fwd_kernel<128, 4>, pdy::FwdCfg<128, 4>::LDS_BYTES)) != hipSuccess)
+      return e;
+    if ((e = set_lds(pdy::fwd_kernel<128, 8>, pdy::FwdCfg<128, 8>::LDS_BYTES)) != hipSuccess)
+      return e;
     if ((e = set_lds(pdy::bwd_dkdv_kernel<64>, pdy::DkdvCfg<64>::LDS_BYTES)) != hipSuccess) return e;
     if ((e = set_lds(pdy::bwd_dkdv_kernel<128>, pdy::DkdvCfg<128>::LDS_BYTES)) != hipSuccess)
       return e;
-    if ((e = set_lds(pdy::bwd_dq_kernel<64>, pdy::DqCfg<64>::LDS_BYTES)) != hipSuccess) return e;
-    if ((e = set_lds(pdy::bwd_dq_kernel<128>, pdy::DqCfg<128>::LDS_BYTES)) != hipSuccess) return e;
+    if ((e = set_lds(pdy::bwd_dq_kernel<64, 4>, pdy::DqCfg<64, 4>::LDS_BYTES)) != hipSuccess)
+      return e;
+    if ((e = set_lds(pdy::bwd_dq_kernel<64, 8>, pdy::DqCfg<64, 8>::LDS_BYTES)) != hipSuccess)
+      return e;
+    if ((e = set_lds(pdy::bwd_dq_kernel<128, 4>, pdy::DqCfg<128, 4>::LDS_BYTES)) != hipSuccess)
+      return e;
+    if ((e = set_lds(pdy::bwd_dq_kernel<128, 8>, pdy::DqCfg<128, 8>::LDS_BYTES)) != hipSuccess)
+      return e;
     return hipSuccess;
   }();
   return status;
+}
+
+template <int D, int NW>
+void launch_fwd(dim3 grid, hipStream_t st, const pdy::FwdArgs& a) {
+  using C = pdy::FwdCfg<D, NW>;
+  hipLaunchKernelGGL((pdy::fwd_kernel<D, NW>), grid, dim3(C::NT), C::LDS_BYTES, st, a);
+}
+
+template <int D, int NW>
+void launch_dq(dim3 grid, hipStream_t st, const pdy::BwdArgs& a) {
+  using C = pdy::DqCfg<D, NW>;
+  hipLaunchKernelGGL((pdy::bwd_dq_kernel<D, NW>), grid, dim3(C::NT), C::LDS_BYTES, st, a);
 }
 
 pdy_status check_scale(float scale, int32_t causal) {
@@ -173,10 +207,12 @@ pdy_status check_ptr(const void* p, const char* name) {
   return PDY_OK;
 }
 
-pdy_status launch_plan(const int32_t* cu, int32_t* ws, const Sizes& s, hipStream_t st) {
+pdy_status launch_plan(const int32_t* cu, int32_t* ws, const Sizes& s, int tile,
+                       hipStream_t st) {
+  const int nt = tiles_of(s, tile);
   hipError_t e = launch_timed(K_PLAN, st, [&] {
     hipLaunchKernelGGL(pdy::plan_kernel, dim3(1), dim3(pdy::kPlanThreads), 0, st, cu, (int)s.N,
-                       kTile, s.max_nt, ws);
+                       tile, nt, ws);
   });
   if (e != hipSuccess) return hip_fail(e, "plan_kernel launch");
   return PDY_OK;
@@ -203,14 +239,14 @@ size_t attn_fwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s);
+  return plan_bytes(s, 32 * fwd_waves(s));
 }
 
 size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s) + dd_bytes(s);
+  return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s);
 }
 
 pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
@@ -232,7 +268,9 @@ pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* 
   if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
   if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
     return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
-  const size_t need = plan_bytes(s);
+  const int nw = fwd_waves(s);
+  const int tile = 32 * nw;
+  const size_t need = plan_bytes(s, tile);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, attn_fwd needs %zu", workspace_bytes,
                 need);
@@ -240,7 +278,7 @@ pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* 
   if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   int32_t* ws = reinterpret_cast<int32_t*>(workspace);
-  if ((st = launch_plan(cu_seqlens, ws, s, hs)) != PDY_OK) return st;
+  if ((st = launch_plan(cu_seqlens, ws, s, tile, hs)) != PDY_OK) return st;
 
   pdy::FwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
@@ -249,20 +287,21 @@ pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* 
   a.cu = cu_seqlens;
   a.o = static_cast<uint16_t*>(o);
   a.lse = lse;
-  a.plan = make_plan(ws, s);
+  a.plan = make_plan(ws, s, tile);
   a.total_tokens = (int)s.T;
   a.hq = (int)s.hq;
   a.hkv = (int)s.hkv;
   a.causal = causal;
   a.scale_log2 = scale * pdy::kLog2e;
-  const dim3 grid((unsigned)(grid_items(s) * s.hq));
+  const dim3 grid((unsigned)(grid_items(s, tile) * s.hq));
   e = launch_timed(K_FWD, hs, [&] {
-    if (s.d == 64)
-      hipLaunchKernelGGL(pdy::fwd_kernel<64>, grid, dim3(pdy::FwdCfg<64>::NT),
-                         pdy::FwdCfg<64>::LDS_BYTES, hs, a);
-    else
-      hipLaunchKernelGGL(pdy::fwd_kernel<128>, grid, dim3(pdy::FwdCfg<128>::NT),
-                         pdy::FwdCfg<128>::LDS_BYTES, hs, a);
+    if (s.d == 64) {
+      if (nw == 8) launch_fwd<64, 8>(grid, hs, a);
+      else launch_fwd<64, 4>(grid, hs, a);
+    } else {
+      if (nw == 8) launch_fwd<128, 8>(grid, hs, a);
+      else launch_fwd<128, 4>(grid, hs, a);
+    }
   });
   if (e != hipSuccess) return hip_fail(e, "fwd_kernel launch");
   return PDY_OK;
@@ -290,7 +329,9 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
   if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
     return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
-  const size_t need = plan_bytes(s) + dd_bytes(s);
+  const int nwq = fwd_waves(s);
+  const int qtile = 32 * nwq;
+  const size_t need = plan_bytes(s, kTile) + plan_bytes(s, qtile) + dd_bytes(s);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, attn_bwd needs %zu", workspace_bytes,
                 need);
@@ -298,9 +339,13 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   int32_t* ws = reinterpret_cast<int32_t*>(workspace);
-  float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) + plan_bytes(s));
+  int32_t* ws_q = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) +
+                                              plan_bytes(s, kTile));
+  float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) +
+                                       plan_bytes(s, kTile) + plan_bytes(s, qtile));
 
-  if ((st = launch_plan(cu_seqlens, ws, s, hs)) != PDY_OK) return st;
+  if ((st = launch_plan(cu_seqlens, ws, s, kTile, hs)) != PDY_OK) return st;
+  if ((st = launch_plan(cu_seqlens, ws_q, s, qtile, hs)) != PDY_OK) return st;
   {
     const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
     const unsigned blocks = (unsigned)((threads + 255) / 256);
@@ -327,16 +372,16 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   a.dq = dq;
   a.dk = dk;
   a.dv = dv;
-  a.plan = make_plan(ws, s);
+  a.plan = make_plan(ws, s, kTile);
+  a.plan_q = make_plan(ws_q, s, qtile);
   a.total_tokens = (int)s.T;
   a.hq = (int)s.hq;
   a.hkv = (int)s.hkv;
   a.causal = causal;
   a.scale = scale;
   a.scale_log2 = scale * pdy::kLog2e;
-  const int64_t items = grid_items(s);
-  const dim3 gkv((unsigned)(items * s.hkv));
-  const dim3 gq((unsigned)(items * s.hq));
+  const dim3 gkv((unsigned)(grid_items(s, kTile) * s.hkv));
+  const dim3 gq((unsigned)(grid_items(s, qtile) * s.hq));
   e = launch_timed(K_DKDV, hs, [&] {
     if (s.d == 64)
       hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
@@ -347,12 +392,13 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   });
   if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
   e = launch_timed(K_DQ, hs, [&] {
-    if (s.d == 64)
-      hipLaunchKernelGGL(pdy::bwd_dq_kernel<64>, gq, dim3(pdy::DqCfg<64>::NT),
-                         pdy::DqCfg<64>::LDS_BYTES, hs, a);
-    else
-      hipLaunchKernelGGL(pdy::bwd_dq_kernel<128>, gq, dim3(pdy::DqCfg<128>::NT),
-                         pdy::DqCfg<128>::LDS_BYTES, hs, a);
+    if (s.d == 64) {
+      if (nwq == 8) launch_dq<64, 8>(gq, hs, a);
+      else launch_dq<64, 4>(gq, hs, a);
+    } else {
+      if (nwq == 8) launch_dq<128, 8>(gq, hs, a);
+      else launch_dq<128, 4>(gq, hs, a);
+    }
   });
   if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
   return PDY_OK;
