@@ -71,20 +71,29 @@ struct BwdArgs {
   float scale_log2;
 };
 
+// dK/dV: one workgroup of 8 waves per (segment, kv head, 128-key tile).  Waves
+// w and w+4 own the same 32 keys (K and V read as B operands from LDS tiles
+// shared by the workgroup) and split every 64-row query step: wave w takes rows
+// 0..31, wave w+4 rows 32..63.  Two waves per SIMD let one wave's softmax
+// recomputation overlap the other's matrix products.  The pair's dK^T/dV^T
+// accumulators are summed through LDS once at the end.
 template <int D>
 struct DkdvCfg {
-  static constexpr int BK = 128;  // keys per workgroup (32 per wave)
-  static constexpr int BQ = 64;   // query rows per step
-  static constexpr int NW = 4;
+  static constexpr int BK = 128;  // keys per workgroup (32 per wave pair)
+  static constexpr int BQ = 64;   // query rows per step (32 per wave)
+  static constexpr int NW = 8;
   static constexpr int NT = NW * 64;
-  static constexpr int TILE = BQ * LdsTile<D>::ROW;
+  static constexpr int TILE = BQ * LdsTile<D>::ROW;  // elements of a Q or dO tile
   // per stage: Q tile, dO tile, lse2[BQ], D[BQ]
   static constexpr int STAGE = 2 * TILE * 2 + 2 * BQ * 4;
-  static constexpr int LDS_BYTES = 2 * STAGE;
+  static constexpr int KVTILE = BK * LdsTile<D>::ROW;  // elements of the K or V tile
+  static constexpr int MAIN_BYTES = 2 * STAGE + 2 * KVTILE * 2;
+  static constexpr int RED_BYTES = 4 * 32 * D * 2 * 4;  // 4 pairs x (dK, dV) fp32
+  static constexpr int LDS_BYTES = MAIN_BYTES > RED_BYTES ? MAIN_BYTES : RED_BYTES;
 };
 
 template <int D>
-__global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
+__global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   using C = DkdvCfg<D>;
   constexpr int BK = C::BK, BQ = C::BQ;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -102,24 +111,14 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
 
   const int l = __lane_id();
   const int w = threadIdx.x >> 6;
+  const int pw = w & 3;    // key block of the pair
+  const int half = w >> 2; // which 32 rows of each step
   const int hh = l >> 5;
-  const int kw0 = k0 + w * 32;         // first key of this wave
+  const int kw0 = k0 + pw * 32;        // first key of this wave
   const int key = kw0 + (l & 31);      // this lane's key
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
 
-  // K^T and V^T as B operands: lane holds K[key][ks*16 + hh*8 + j]
-  bf16x8 kf[D / 16], vf[D / 16];
-  {
-    const bool ok = key < seg_hi;
-    const uint16_t* kp = a.k + (size_t)key * kvstride + (size_t)hk * D + hh * 8;
-    const uint16_t* vp = a.v + (size_t)key * kvstride + (size_t)hk * D + hh * 8;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      kf[ks] = load_bf16x8(kp + ks * 16, ok);
-      vf[ks] = load_bf16x8(vp + ks * 16, ok);
-    }
-  }
   f32x16 dka[D / 32], dva[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) {
@@ -127,38 +126,47 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
     dva[i] = zero16();
   }
 
+  uint8_t* const base = reinterpret_cast<uint8_t*>(smem);
+  uint16_t* const ktile_s = reinterpret_cast<uint16_t*>(base + 2 * C::STAGE);
+  uint16_t* const vtile = ktile_s + C::KVTILE;
+  {
+    // K and V tiles (keys past the segment end repeat the last key; their
+    // gradients are never written out)
+    TileLoader<BK, D, C::NT> kl, vl;
+    kl.load_clamped(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
+    vl.load_clamped(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
+    kl.store(ktile_s);
+    vl.store(vtile);
+  }
+
   // query rows that can see this key tile
   const int qstart = a.causal ? k0 : seg_lo;
   const int nqt = (seg_hi - qstart + BQ - 1) / BQ;
   const int nsteps = nqt * g;
 
-  auto stage_ptr = [&](int buf) { return reinterpret_cast<uint8_t*>(smem) + buf * C::STAGE; };
-
   TileLoader<BQ, D, C::NT> ql, gl;
-  float lse_r = 0.f, dd_r = 0.f;  // one row per thread (threads 0..BQ-1)
+  float stat = 0.f;  // threads 0..BQ-1: lse2 of a row; BQ..2BQ-1: D of a row
   auto issue = [&](int step) {
     const int hi = step / nqt;
     const int qi = step % nqt;
     const int h = hk * g + hi;
     const int r0 = qstart + qi * BQ;
-    ql.load(a.q + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
-    gl.load(a.dout + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
-    if (threadIdx.x < BQ) {
-      const int r = r0 + threadIdx.x;
+    // rows past the segment end repeat the last row; they are always masked
+    ql.load_clamped(a.q + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
+    gl.load_clamped(a.dout + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
+    const int t = threadIdx.x;
+    if (t < 2 * BQ) {
+      const int r = r0 + (t % BQ);
       const bool ok = r < seg_hi;
-      lse_r = ok ? a.lse[(size_t)h * a.total_tokens + r] * kLog2e : 0.f;
-      dd_r = ok ? a.dd[(size_t)h * a.total_tokens + r] : 0.f;
+      const size_t idx = (size_t)h * a.total_tokens + r;
+      stat = ok ? (t < BQ ? a.lse[idx] * kLog2e : a.dd[idx]) : 0.f;
     }
   };
   auto commit = [&](int buf) {
-    uint8_t* st = stage_ptr(buf);
+    uint8_t* st = base + buf * C::STAGE;
     ql.store(reinterpret_cast<uint16_t*>(st));
     gl.store(reinterpret_cast<uint16_t*>(st) + C::TILE);
-    float* stats = reinterpret_cast<float*>(st + 2 * C::TILE * 2);
-    if (threadIdx.x < BQ) {
-      stats[threadIdx.x] = lse_r;
-      stats[BQ + threadIdx.x] = dd_r;
-    }
+    if (threadIdx.x < 2 * BQ) reinterpret_cast<float*>(st + 2 * C::TILE * 2)[threadIdx.x] = stat;
   };
 
   if (nsteps > 0) {
@@ -169,62 +177,75 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
     const bool more = step + 1 < nsteps;
     if (more) issue(step + 1);
     __syncthreads();
-    const uint8_t* st = stage_ptr(step & 1);
+    const uint8_t* st = base + (step & 1) * C::STAGE;
     const uint16_t* qs = reinterpret_cast<const uint16_t*>(st);
     const uint16_t* gs = qs + C::TILE;
     const float* lse_s = reinterpret_cast<const float*>(st + 2 * C::TILE * 2);
     const float* dd_s = lse_s + BQ;
-    const int r0 = qstart + (step % nqt) * BQ;
+    const int wr0 = qstart + (step % nqt) * BQ + half * 32;  // first row of this wave
 
-    const bool active = (kw0 < seg_hi) && (!a.causal || r0 + BQ - 1 >= kw0);
+    const bool active = (kw0 < seg_hi) && (wr0 < seg_hi) && (!a.causal || wr0 + 31 >= kw0);
     if (active) {
-      const bool need_mask = (a.causal && r0 < kw0 + 31) || (r0 + BQ > seg_hi);
-      f32x16 p[BQ / 32], ds[BQ / 32];
+      const bool need_mask = (a.causal && wr0 < kw0 + 31) || (wr0 + 32 > seg_hi);
+      // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows
+      f32x16 s = zero16(), dp = zero16();
 #pragma unroll
-      for (int rb = 0; rb < BQ / 32; ++rb) {
-        // S[row][key] = Q K^T : A = Q rows from LDS, B = K^T registers
-        f32x16 s = zero16();
-        f32x16 dp = zero16();
+      for (int ks = 0; ks < D / 16; ++ks) {
+        s = mfma32(lds_row_operand<D>(qs, half * 32, ks * 16),
+                   lds_row_operand<D>(ktile_s, pw * 32, ks * 16), s);
+        dp = mfma32(lds_row_operand<D>(gs, half * 32, ks * 16),
+                    lds_row_operand<D>(vtile, pw * 32, ks * 16), dp);
+      }
+      // causal: key visible to row iff row - (wr0 + hh*4) >= key - (wr0 + hh*4)
+      const int rel = key - wr0 - hh * 4;
+      const int rows_left = seg_hi - wr0 - hh * 4;
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(lds_row_operand<D>(qs, rb * 32, ks * 16), kf[ks], s);
-          dp = mfma32(lds_row_operand<D>(gs, rb * 32, ks * 16), vf[ks], dp);
-        }
+      for (int grp = 0; grp < 4; ++grp) {
+        const int rl = half * 32 + grp * 8 + hh * 4;
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rl);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(dd_s + rl);
 #pragma unroll
-        for (int grp = 0; grp < 4; ++grp) {
-          const int rl = rb * 32 + grp * 8 + hh * 4;  // local row of r = grp*4
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rl);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(dd_s + rl);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = grp * 4 + e;
-            float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -l4[e]));
-            if (need_mask) {
-              const int row = r0 + rl + e;
-              const bool vis = row < seg_hi && key < seg_hi && (!a.causal || key <= row);
-              if (!vis) pv = 0.f;
-            }
-            p[rb][r] = pv;
-            ds[rb][r] = pv * (dp[r] - d4[e]);
+        for (int e = 0; e < 4; ++e) {
+          const int r = grp * 4 + e;
+          float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -l4[e]));
+          if (need_mask) {
+            const int off = acc_row_off(r);
+            if ((a.causal && off < rel) || off >= rows_left) pv = 0.f;
           }
+          s[r] = pv;
+          dp[r] = pv * (dp[r] - d4[e]);  // dS
         }
       }
-      // dV^T += dO^T P  and  dK^T += Q^T dS  over 4 row steps of 16
+      // dV^T += dO^T P  and  dK^T += Q^T dS over two 16-row steps
 #pragma unroll
-      for (int t = 0; t < BQ / 16; ++t) {
-        bf16x8 pb = pack8(p[t >> 1], (t & 1) * 8);
-        bf16x8 sb = pack8(ds[t >> 1], (t & 1) * 8);
+      for (int t2 = 0; t2 < 2; ++t2) {
+        const bf16x8 pb = pack8(s, t2 * 8);
+        const bf16x8 sb = pack8(dp, t2 * 8);
+        const int r16 = half * 32 + t2 * 16;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          dva[db] = mfma32(lds_tr_a_operand<D>(gs, t * 16, db * 32), pb, dva[db]);
-          dka[db] = mfma32(lds_tr_a_operand<D>(qs, t * 16, db * 32), sb, dka[db]);
+          dva[db] = mfma32(lds_tr_a_operand<D>(gs, r16, db * 32), pb, dva[db]);
+          dka[db] = mfma32(lds_tr_a_operand<D>(qs, r16, db * 32), sb, dka[db]);
         }
       }
     }
     if (more) commit((step + 1) & 1);
   }
 
-  if (key < seg_hi) {
+  // sum the pair's accumulators: waves 4..7 park theirs in LDS
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(base) + pw * (32 * D * 2);
+  if (half == 1) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        red[(db * 16 + r) * 64 + l] = dka[db][r];
+        red[32 * D + (db * 16 + r) * 64 + l] = dva[db][r];
+      }
+  }
+  __syncthreads();
+  if (half == 0 && key < seg_hi) {
     float* dkp = a.dk + (size_t)key * kvstride + (size_t)hk * D;
     float* dvp = a.dv + (size_t)key * kvstride + (size_t)hk * D;
 #pragma unroll
@@ -232,10 +253,13 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
         const int d0 = db * 32 + grp * 8 + hh * 4;
-        f32x4 kv = {dka[db][grp * 4] * a.scale, dka[db][grp * 4 + 1] * a.scale,
-                    dka[db][grp * 4 + 2] * a.scale, dka[db][grp * 4 + 3] * a.scale};
-        f32x4 vv = {dva[db][grp * 4], dva[db][grp * 4 + 1], dva[db][grp * 4 + 2],
-                    dva[db][grp * 4 + 3]};
+        f32x4 kv, vv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = grp * 4 + e;
+          kv[e] = (dka[db][r] + red[(db * 16 + r) * 64 + l]) * a.scale;
+          vv[e] = dva[db][r] + red[32 * D + (db * 16 + r) * 64 + l];
+        }
         *reinterpret_cast<f32x4*>(dkp + d0) = kv;
         *reinterpret_cast<f32x4*>(dvp + d0) = vv;
       }
