@@ -1,0 +1,112 @@
+"""The C-ABI library loads without a GPU, exports every function the header
+declares, and rejects bad arguments before touching HIP."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2511_13198_amd import pdyattn as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pdyattn.h")
+
+FAKE = 0x10000  # aligned, never dereferenced: every call below fails validation first
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"defined"})
+
+
+def test_header_symbols_exported():
+    names = header_functions()
+    assert "attn_fwd" in names and "attn_bwd" in names
+    L = P.lib()
+    missing = [n for n in names if not hasattr(L, n)]
+    assert not missing, f"missing exports: {missing}"
+    assert sorted(P.SYMBOLS) == names
+
+
+def _fwd(**kw):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, cu=FAKE, n=1, T=512, maxlen=512, hq=8, hkv=8, d=128,
+                causal=1, scale=0.1, o=FAKE, lse=FAKE, ws=FAKE, wsb=1 << 20, stream=None)
+    args.update(kw)
+    return P.lib().attn_fwd(args["q"], args["k"], args["v"], args["cu"], args["n"], args["T"],
+                            args["maxlen"], args["hq"], args["hkv"], args["d"], args["causal"],
+                            args["scale"], args["o"], args["lse"], args["ws"], args["wsb"],
+                            args["stream"])
+
+
+def _bwd(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, do=FAKE, cu=FAKE, n=1, T=512, maxlen=512,
+             hq=8, hkv=8, d=128, causal=1, scale=0.1, dq=FAKE, dk=FAKE, dv=FAKE, ws=FAKE,
+             wsb=1 << 30, stream=None)
+    a.update(kw)
+    return P.lib().attn_bwd(a["q"], a["k"], a["v"], a["o"], a["lse"], a["do"], a["cu"], a["n"],
+                            a["T"], a["maxlen"], a["hq"], a["hkv"], a["d"], a["causal"],
+                            a["scale"], a["dq"], a["dk"], a["dv"], a["ws"], a["wsb"],
+                            a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(d=96), P.PDY_ERR_UNSUPPORTED, "head_dim"),
+    (dict(hq=6, hkv=4), P.PDY_ERR_INVALID_ARG, "multiple"),
+    (dict(hkv=0), P.PDY_ERR_INVALID_ARG, "head counts"),
+    (dict(n=0), P.PDY_ERR_INVALID_ARG, "num_seqs"),
+    (dict(T=-1), P.PDY_ERR_INVALID_ARG, "total_tokens"),
+    (dict(maxlen=513), P.PDY_ERR_INVALID_ARG, "max_seqlen"),
+    (dict(maxlen=0), P.PDY_ERR_INVALID_ARG, "max_seqlen"),
+    (dict(causal=2), P.PDY_ERR_INVALID_ARG, "causal"),
+    (dict(scale=0.0), P.PDY_ERR_INVALID_ARG, "scale"),
+    (dict(scale=float("nan")), P.PDY_ERR_INVALID_ARG, "scale"),
+    (dict(q=0), P.PDY_ERR_INVALID_ARG, "q is NULL"),
+    (dict(o=FAKE + 8), P.PDY_ERR_INVALID_ARG, "aligned"),
+    (dict(cu=0), P.PDY_ERR_INVALID_ARG, "cu_seqlens"),
+    (dict(cu=FAKE + 2), P.PDY_ERR_INVALID_ARG, "cu_seqlens"),
+    (dict(wsb=16), P.PDY_ERR_WORKSPACE, "workspace"),
+])
+def test_fwd_argument_errors(kw, status, msg):
+    st = _fwd(**kw)
+    assert st == status, (st, P.last_error())
+    assert msg in P.last_error()
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(d=32), P.PDY_ERR_UNSUPPORTED, "head_dim"),
+    (dict(dk=0), P.PDY_ERR_INVALID_ARG, "dk is NULL"),
+    (dict(do=FAKE + 4), P.PDY_ERR_INVALID_ARG, "aligned"),
+    (dict(wsb=1024), P.PDY_ERR_WORKSPACE, "workspace"),
+    (dict(hq=32, hkv=5), P.PDY_ERR_INVALID_ARG, "multiple"),
+])
+def test_bwd_argument_errors(kw, status, msg):
+    st = _bwd(**kw)
+    assert st == status, (st, P.last_error())
+    assert msg in P.last_error()
+
+
+def test_empty_batch_is_noop():
+    # T = 0 returns before any pointer check or launch
+    assert _fwd(T=0, maxlen=0, q=0, k=0, v=0, o=0, lse=0, ws=0, wsb=0) == P.PDY_OK
+    assert _bwd(T=0, maxlen=0, q=0) == P.PDY_OK
+
+
+def test_workspace_sizes():
+    f = P.fwd_workspace_size(65536, 25, 7402, 32, 32, 128)
+    b = P.bwd_workspace_size(65536, 25, 7402, 32, 32, 128)
+    assert 256 <= f < 1 << 20
+    assert b >= 32 * 65536 * 4  # D = rowsum(dO*O), fp32 [Hq, T]
+    assert P.fwd_workspace_size(512, 1, 512, 8, 8, 96) == 0
+    assert P.bwd_workspace_size(512, 1, 513, 8, 8, 128) == 0
+
+
+def test_status_strings_and_kernel_names():
+    L = P.lib()
+    assert L.pdy_status_string(0) == b"ok"
+    assert L.pdy_status_string(-3) == b"workspace too small"
+    names = [L.pdy_kernel_name(i).decode() for i in range(L.pdy_kernel_count())]
+    assert {"fwd_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel"} <= set(names)
+    # profiling with nothing launched reports nothing
+    P.profile_start()
+    assert P.profile_stop() == {}
