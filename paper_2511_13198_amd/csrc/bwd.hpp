@@ -83,11 +83,13 @@ struct DkdvCfg {
   static constexpr int BQ = 64;   // query rows per step (32 per wave)
   static constexpr int NW = 8;
   static constexpr int NT = NW * 64;
-  static constexpr int TILE = BQ * LdsTile<D>::ROW;  // elements of a Q or dO tile
+  using QL = DualLayout<D>;  // Q and dO: read as rows (S, dP) and transposed (dK, dV)
+  using KL = RowsLayout<D>;  // K and V: read as rows only
+  static constexpr int QTILE = QL::elems(BQ);
+  static constexpr int KTILE = KL::elems(BK);
   // per stage: Q tile, dO tile, lse2[BQ], D[BQ]
-  static constexpr int STAGE = 2 * TILE * 2 + 2 * BQ * 4;
-  static constexpr int KVTILE = BK * LdsTile<D>::ROW;  // elements of the K or V tile
-  static constexpr int MAIN_BYTES = 2 * STAGE + 2 * KVTILE * 2;
+  static constexpr int STAGE = 2 * QTILE * 2 + 2 * BQ * 4;
+  static constexpr int MAIN_BYTES = 2 * STAGE + 2 * KTILE * 2;
   static constexpr int RED_BYTES = 4 * 32 * D * 2 * 4;  // 4 pairs x (dK, dV) fp32
   static constexpr int LDS_BYTES = MAIN_BYTES > RED_BYTES ? MAIN_BYTES : RED_BYTES;
 };
@@ -95,7 +97,9 @@ struct DkdvCfg {
 template <int D>
 __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   using C = DkdvCfg<D>;
-  constexpr int BK = C::BK, BQ = C::BQ;
+  using QL = typename C::QL;
+  using KL = typename C::KL;
+  constexpr int BK = C::BK, BQ = C::BQ, NW = C::NW;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   const int item = blockIdx.x / a.hkv;
@@ -128,108 +132,180 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
 
   uint8_t* const base = reinterpret_cast<uint8_t*>(smem);
   uint16_t* const ktile_s = reinterpret_cast<uint16_t*>(base + 2 * C::STAGE);
-  uint16_t* const vtile = ktile_s + C::KVTILE;
-  {
-    // K and V tiles (keys past the segment end repeat the last key; their
-    // gradients are never written out)
-    TileLoader<BK, D, C::NT> kl, vl;
-    kl.load_clamped(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
-    vl.load_clamped(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
-    kl.store(ktile_s);
-    vl.store(vtile);
-  }
+  uint16_t* const vtile = ktile_s + C::KTILE;
+  auto qbuf = [&](int b) __attribute__((always_inline)) {
+    return reinterpret_cast<uint16_t*>(base + b * C::STAGE);
+  };
+  auto gbuf = [&](int b) __attribute__((always_inline)) { return qbuf(b) + C::QTILE; };
+  auto stats = [&](int b) __attribute__((always_inline)) {
+    return reinterpret_cast<float*>(base + b * C::STAGE + 2 * C::QTILE * 2);
+  };
 
   // query rows that can see this key tile
   const int qstart = a.causal ? k0 : seg_lo;
   const int nqt = (seg_hi - qstart + BQ - 1) / BQ;
   const int nsteps = nqt * g;
 
-  TileLoader<BQ, D, C::NT> ql, gl;
   float stat = 0.f;  // threads 0..BQ-1: lse2 of a row; BQ..2BQ-1: D of a row
-  auto issue = [&](int step) {
-    const int hi = step / nqt;
-    const int qi = step % nqt;
-    const int h = hk * g + hi;
-    const int r0 = qstart + qi * BQ;
-    // rows past the segment end repeat the last row; they are always masked
-    ql.load_clamped(a.q + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
-    gl.load_clamped(a.dout + (size_t)r0 * qstride + (size_t)h * D, qstride, seg_hi - r0);
+  auto load_stat = [&](int step) __attribute__((always_inline)) {
     const int t = threadIdx.x;
     if (t < 2 * BQ) {
-      const int r = r0 + (t % BQ);
+      const int h = hk * g + step / nqt;
+      const int r = qstart + (step % nqt) * BQ + (t % BQ);
       const bool ok = r < seg_hi;
       const size_t idx = (size_t)h * a.total_tokens + r;
       stat = ok ? (t < BQ ? a.lse[idx] * kLog2e : a.dd[idx]) : 0.f;
     }
   };
-  auto commit = [&](int buf) {
-    uint8_t* st = base + buf * C::STAGE;
-    ql.store(reinterpret_cast<uint16_t*>(st));
-    gl.store(reinterpret_cast<uint16_t*>(st) + C::TILE);
-    if (threadIdx.x < 2 * BQ) reinterpret_cast<float*>(st + 2 * C::TILE * 2)[threadIdx.x] = stat;
+  auto store_stat = [&](int b) __attribute__((always_inline)) {
+    if (threadIdx.x < 2 * BQ) stats(b)[threadIdx.x] = stat;
   };
 
-  if (nsteps > 0) {
-    issue(0);
-    commit(0);
-  }
-  for (int step = 0; step < nsteps; ++step) {
-    const bool more = step + 1 < nsteps;
-    if (more) issue(step + 1);
-    __syncthreads();
-    const uint8_t* st = base + (step & 1) * C::STAGE;
-    const uint16_t* qs = reinterpret_cast<const uint16_t*>(st);
-    const uint16_t* gs = qs + C::TILE;
-    const float* lse_s = reinterpret_cast<const float*>(st + 2 * C::TILE * 2);
+  const int q_row = row_lane_base<QL>();
+  const int q_tr = tr_lane_base<QL>();
+  const int k_row = row_lane_base<KL>();
+  const uint16_t* const kp = ktile_s + k_row;
+  const uint16_t* const vp = vtile + k_row;
+
+  auto compute = [&](int step) __attribute__((always_inline)) {
+    const int b = step & 1;
+    const uint16_t* qs = qbuf(b);
+    const uint16_t* gs = gbuf(b);
+    const float* lse_s = stats(b);
     const float* dd_s = lse_s + BQ;
     const int wr0 = qstart + (step % nqt) * BQ + half * 32;  // first row of this wave
-
     const bool active = (kw0 < seg_hi) && (wr0 < seg_hi) && (!a.causal || wr0 + 31 >= kw0);
-    if (active) {
-      const bool need_mask = (a.causal && wr0 < kw0 + 31) || (wr0 + 32 > seg_hi);
-      // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows
-      f32x16 s = zero16(), dp = zero16();
+    if (!active) return;
+    const bool need_mask = (a.causal && wr0 < kw0 + 31) || (wr0 + 32 > seg_hi);
+    // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows
+    f32x16 s = zero16(), dp = zero16();
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        s = mfma32(lds_row_operand<D>(qs, half * 32, ks * 16),
-                   lds_row_operand<D>(ktile_s, pw * 32, ks * 16), s);
-        dp = mfma32(lds_row_operand<D>(gs, half * 32, ks * 16),
-                    lds_row_operand<D>(vtile, pw * 32, ks * 16), dp);
-      }
+    for (int ks = 0; ks < D / 16; ++ks) {
+      s = mfma32(lds_row_operand<QL>(qs + q_row, half * 32, ks * 16),
+                 lds_row_operand<KL>(kp, pw * 32, ks * 16), s);
+      dp = mfma32(lds_row_operand<QL>(gs + q_row, half * 32, ks * 16),
+                  lds_row_operand<KL>(vp, pw * 32, ks * 16), dp);
+    }
+    if (need_mask) {  // diagonal or segment-end step only
       // causal: key visible to row iff row - (wr0 + hh*4) >= key - (wr0 + hh*4)
-      const int rel = key - wr0 - hh * 4;
+      const int rel = a.causal ? key - wr0 - hh * 4 : -32;
       const int rows_left = seg_hi - wr0 - hh * 4;
 #pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        const int rl = half * 32 + grp * 8 + hh * 4;
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rl);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(dd_s + rl);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = grp * 4 + e;
-          float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -l4[e]));
-          if (need_mask) {
-            const int off = acc_row_off(r);
-            if ((a.causal && off < rel) || off >= rows_left) pv = 0.f;
-          }
-          s[r] = pv;
-          dp[r] = pv * (dp[r] - d4[e]);  // dS
-        }
-      }
-      // dV^T += dO^T P  and  dK^T += Q^T dS over two 16-row steps
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        const bf16x8 pb = pack8(s, t2 * 8);
-        const bf16x8 sb = pack8(dp, t2 * 8);
-        const int r16 = half * 32 + t2 * 16;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          dva[db] = mfma32(lds_tr_a_operand<D>(gs, r16, db * 32), pb, dva[db]);
-          dka[db] = mfma32(lds_tr_a_operand<D>(qs, r16, db * 32), sb, dka[db]);
-        }
+      for (int r = 0; r < 16; ++r) {
+        const int off = acc_row_off(r);
+        if (off < rel || off >= rows_left) s[r] = -INFINITY;
       }
     }
-    if (more) commit((step + 1) & 1);
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+      const int rl = half * 32 + grp * 8 + hh * 4;
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rl);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(dd_s + rl);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = grp * 4 + e;
+        const float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -l4[e]));
+        s[r] = pv;
+        dp[r] = pv * (dp[r] - d4[e]);  // dS
+      }
+    }
+    // dV^T += dO^T P  and  dK^T += Q^T dS over two 16-row steps; the
+    // transposing reads of the next product are in flight during each one
+    constexpr int NDB = D / 32;
+    const uint32_t ga = lds_addr(gs) + (q_tr + half * 32 * QL::ROW) * 2;
+    const uint32_t qa = lds_addr(qs) + (q_tr + half * 32 * QL::ROW) * 2;
+    TrRegs ra[NDB], rb[NDB];
+    static_for<NDB>([&](auto DB) { tr_issue<QL, 0, DB * 32>(ga, ra[DB]); });
+    static_for<NDB>([&](auto DB) { tr_issue<QL, 0, DB * 32>(qa, rb[DB]); });
+    const bf16x8 pb0 = pack8(s, 0), sb0 = pack8(dp, 0);
+    tr_wait<2 * NDB>(ra);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) dva[db] = mfma32(ra[db].operand(), pb0, dva[db]);
+    static_for<NDB>([&](auto DB) { tr_issue<QL, 16, DB * 32>(ga, ra[DB]); });
+    tr_wait<2 * NDB>(rb);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) dka[db] = mfma32(rb[db].operand(), sb0, dka[db]);
+    static_for<NDB>([&](auto DB) { tr_issue<QL, 16, DB * 32>(qa, rb[DB]); });
+    const bf16x8 pb1 = pack8(s, 8), sb1 = pack8(dp, 8);
+    tr_wait<2 * NDB>(ra);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) dva[db] = mfma32(ra[db].operand(), pb1, dva[db]);
+    tr_wait<0>(rb);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) dka[db] = mfma32(rb[db].operand(), sb1, dka[db]);
+  };
+
+  auto row_ptr = [&](const uint16_t* t, int step) __attribute__((always_inline)) {
+    const int h = hk * g + step / nqt;
+    const int r0 = qstart + (step % nqt) * BQ;
+    return t + (size_t)r0 * qstride + (size_t)h * D;
+  };
+  auto rows_valid = [&](int step) __attribute__((always_inline)) {
+    return seg_hi - (qstart + (step % nqt) * BQ);
+  };
+
+  // K and V tiles (keys past the segment end repeat the last key; their
+  // gradients are never written out); query-side tiles repeat the last row
+  // past the segment end and are masked.
+  if constexpr (D == 128) {
+    {
+      TileDma<KL, BK, NW> kvd;
+      kvd.init(kvstride);
+      kvd.issue(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0, ktile_s);
+      kvd.issue(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0, vtile);
+    }
+    TileDma<QL, BQ, NW> qd;
+    qd.init(qstride);
+    auto issue = [&](int step) __attribute__((always_inline)) {
+      qd.issue(row_ptr(a.q, step), qstride, rows_valid(step), qbuf(step & 1));
+      qd.issue(row_ptr(a.dout, step), qstride, rows_valid(step), gbuf(step & 1));
+    };
+    if (nsteps > 0) {
+      issue(0);
+      load_stat(0);
+      store_stat(0);
+    }
+    for (int step = 0; step < nsteps; ++step) {
+      const bool more = step + 1 < nsteps;
+      wait_dma();
+      __syncthreads();
+      if (more) {
+        issue(step + 1);
+        load_stat(step + 1);
+      }
+      compute(step);
+      if (more) store_stat((step + 1) & 1);
+    }
+  } else {
+    {
+      TileLoader<KL, BK, D, C::NT> kl, vl;
+      kl.load_clamped(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
+      vl.load_clamped(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
+      kl.store(ktile_s);
+      vl.store(vtile);
+    }
+    TileLoader<QL, BQ, D, C::NT> ql, gl;
+    auto issue = [&](int step) __attribute__((always_inline)) {
+      ql.load_clamped(row_ptr(a.q, step), qstride, rows_valid(step));
+      gl.load_clamped(row_ptr(a.dout, step), qstride, rows_valid(step));
+      load_stat(step);
+    };
+    auto commit = [&](int b) __attribute__((always_inline)) {
+      ql.store(qbuf(b));
+      gl.store(gbuf(b));
+      store_stat(b);
+    };
+    if (nsteps > 0) {
+      issue(0);
+      commit(0);
+    }
+    for (int step = 0; step < nsteps; ++step) {
+      const bool more = step + 1 < nsteps;
+      if (more) issue(step + 1);
+      __syncthreads();
+      compute(step);
+      if (more) commit((step + 1) & 1);
+    }
   }
 
   // sum the pair's accumulators: waves 4..7 park theirs in LDS
@@ -271,13 +347,18 @@ struct DqCfg {
   static constexpr int BQ = 32 * NW;
   static constexpr int BK = 64;
   static constexpr int NT = NW * 64;
-  static constexpr int TILE = BK * LdsTile<D>::ROW;
-  static constexpr int LDS_BYTES = 2 * 2 * TILE * 2;
+  using KL = DualLayout<D>;  // K is read as rows (S^T) and transposed (dQ^T)
+  using VL = RowsLayout<D>;  // V is read as rows (dP^T)
+  static constexpr int KTILE = KL::elems(BK);
+  static constexpr int VTILE = VL::elems(BK);
+  static constexpr int LDS_BYTES = 2 * (KTILE + VTILE) * 2;
 };
 
 template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) bwd_dq_kernel(BwdArgs a) {
   using C = DqCfg<D, NW>;
+  using KL = typename C::KL;
+  using VL = typename C::VL;
   constexpr int BQ = C::BQ, BK = C::BK;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
@@ -322,59 +403,101 @@ __global__ void __launch_bounds__(NW * 64) bwd_dq_kernel(BwdArgs a) {
 
   const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
   const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
-  // buffer b: K at smem + 2*b*TILE, V right after it
-  auto kbuf = [&](int b) { return smem + 2 * b * C::TILE; };
-  auto vbuf = [&](int b) { return smem + (2 * b + 1) * C::TILE; };
-  TileLoader<BK, D, C::NT> kl, vl;
+  auto kbuf = [&](int t) __attribute__((always_inline)) { return smem + (t & 1) * C::KTILE; };
+  auto vbuf = [&](int t) __attribute__((always_inline)) {
+    return smem + 2 * C::KTILE + (t & 1) * C::VTILE;
+  };
+  const int k_row = row_lane_base<KL>();
+  const int k_tr = tr_lane_base<KL>();
+  const int v_row = row_lane_base<VL>();
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  // rows past the segment end repeat the last key; they are always masked
-  kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-  vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-  kl.store(kbuf(0));
-  vl.store(vbuf(0));
-  for (int it = 0; it < ntiles; ++it) {
+
+  auto compute = [&](int it) __attribute__((always_inline)) {
     const int k0 = seg_lo + it * BK;
-    const bool more = it + 1 < ntiles;
-    if (more) {
-      const int k1 = k0 + BK;
-      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-    }
-    __syncthreads();
-    const uint16_t* ks_ = kbuf(it & 1);
-    const uint16_t* vs_ = vbuf(it & 1);
     const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
-    if (active) {
-      const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
-      // one 32-key block at a time keeps S^T and dP^T to 32 registers
+    if (!active) return;
+    const uint16_t* kp = kbuf(it) + k_row;
+    const uint32_t ka = lds_addr(kbuf(it)) + k_tr * 2;
+    const uint16_t* vp = vbuf(it) + v_row;
+    const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
+    // one 32-key block at a time keeps S^T and dP^T to 32 registers
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) {
-        f32x16 s = zero16(), dp = zero16();
+    for (int kb = 0; kb < BK / 32; ++kb) {
+      f32x16 s = zero16(), dp = zero16();
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(lds_row_operand<D>(ks_, kb * 32, ks * 16), qf[ks], s);
-          dp = mfma32(lds_row_operand<D>(vs_, kb * 32, ks * 16), gf[ks], dp);
-        }
+      for (int ks = 0; ks < D / 16; ++ks) {
+        s = mfma32(lds_row_operand<KL>(kp, kb * 32, ks * 16), qf[ks], s);
+        dp = mfma32(lds_row_operand<VL>(vp, kb * 32, ks * 16), gf[ks], dp);
+      }
+      if (need_mask) {  // diagonal or segment-end tile only
         const int lim = key_lim - (k0 + kb * 32 + hh * 4);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -lse2));
-          if (need_mask && acc_row_off(r) > lim) pv = 0.f;
-          s[r] = pv * (dp[r] - ddv);  // dS^T
-        }
-#pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
-          const bf16x8 sb = pack8(s, t2 * 8);
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db)
-            dqa[db] = mfma32(lds_tr_a_operand<D>(ks_, kb * 32 + t2 * 16, db * 32), sb, dqa[db]);
-        }
+        for (int r = 0; r < 16; ++r)
+          if (acc_row_off(r) > lim) s[r] = -INFINITY;
       }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pv = fast_exp2(__builtin_fmaf(s[r], a.scale_log2, -lse2));
+        s[r] = pv * (dp[r] - ddv);  // dS^T
+      }
+      // dQ^T += K^T dS^T for the block's two 16-key steps
+      constexpr int NDB = D / 32;
+      TrRegs kt0[NDB], kt1[NDB];
+      // all of kt0 is issued before kt1, so "at most 2*NDB outstanding" means
+      // kt0 has landed
+      const uint32_t kab = ka + kb * 32 * KL::ROW * 2;
+      static_for<NDB>([&](auto DB) { tr_issue<KL, 0, DB * 32>(kab, kt0[DB]); });
+      static_for<NDB>([&](auto DB) { tr_issue<KL, 16, DB * 32>(kab, kt1[DB]); });
+      tr_wait<2 * NDB>(kt0);
+      const bf16x8 sb0 = pack8(s, 0);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) dqa[db] = mfma32(kt0[db].operand(), sb0, dqa[db]);
+      tr_wait<0>(kt1);
+      const bf16x8 sb1 = pack8(s, 8);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) dqa[db] = mfma32(kt1[db].operand(), sb1, dqa[db]);
     }
-    if (more) {
-      kl.store(kbuf((it + 1) & 1));
-      vl.store(vbuf((it + 1) & 1));
+  };
+
+  // rows past the segment end repeat the last key; they are always masked
+  if constexpr (D == 128) {
+    TileDma<KL, BK, NW> kd;
+    TileDma<VL, BK, NW> vd;
+    kd.init(kvstride);
+    vd.init(kvstride);
+    auto issue = [&](int t) __attribute__((always_inline)) {
+      const int kt = seg_lo + t * BK;
+      kd.issue(kbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, kbuf(t));
+      vd.issue(vbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, vbuf(t));
+    };
+    issue(0);
+    for (int it = 0; it < ntiles; ++it) {
+      wait_dma();
+      __syncthreads();
+      if (it + 1 < ntiles) issue(it + 1);
+      compute(it);
+    }
+  } else {
+    TileLoader<KL, BK, D, C::NT> kl;
+    TileLoader<VL, BK, D, C::NT> vl;
+    kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+    vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+    kl.store(kbuf(0));
+    vl.store(vbuf(0));
+    for (int it = 0; it < ntiles; ++it) {
+      const bool more = it + 1 < ntiles;
+      if (more) {
+        const int k1 = seg_lo + (it + 1) * BK;
+        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      }
+      __syncthreads();
+      compute(it);
+      if (more) {
+        kl.store(kbuf(it + 1));
+        vl.store(vbuf(it + 1));
+      }
     }
   }
 

@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace pdy {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -29,6 +31,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = 0..N-1.
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
+// LDS byte address of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(p);
+}
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -74,54 +90,89 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p, bool valid) {
 }
 
 // ---------------------------------------------------------------------------
-// LDS tile layout.  A tile holds rows of D bf16 values as 16-byte chunks.
-// For D = 128 a row is exactly 256 bytes (all 64 banks) and chunk c of row r
-// is stored at chunk position c ^ swz(r), swz(r) = 4*(r % 4) + (r / 4) % 4.
-// That makes both access patterns below conflict-free:
-//   * row reads (16 lanes = 16 consecutive rows, one chunk each): swz is a
-//     bijection on any 16 consecutive rows aligned to 16;
-//   * transposing reads (32 lanes = 4 consecutive rows x 4 consecutive
-//     chunks, rows and chunks aligned to 4): the low two bits of the
-//     position come from the chunk, the high two from the row.
-// For D = 64 rows are padded to 72 elements instead.
+// LDS tile layouts.  A tile holds rows of D bf16 values as 16-byte chunks; all
+// offsets below are in bf16 elements.  Two access patterns occur:
+//   * row reads (lds_row_operand): a quarter-wave reads the same chunk of 16
+//     consecutive rows;
+//   * transposing reads (lds_tr_operand): a half-wave reads 4 consecutive rows
+//     x 64 consecutive bytes.
+// RowsLayout pads rows to D + 8 elements (272 B for D = 128), which makes row
+// reads conflict-free.  DualLayout (D = 128) stores row r at 320 r bytes
+// shifted by 16 ((r / 4) mod 4) bytes; its bank pattern 4 (r mod 4) +
+// (r / 4) mod 4 (in 16-byte units) makes both patterns conflict-free, and in
+// both layouts an operand's address is one per-lane base plus an immediate.
+// For D = 64 DualLayout falls back to RowsLayout.
 // ---------------------------------------------------------------------------
 template <int D>
-struct LdsTile {
-  static constexpr int ROW = (D == 128) ? 128 : D + 8;  // elements per stored row
-  __device__ __forceinline__ static int off(int r, int chunk) {
-    if constexpr (D == 128) return r * 128 + ((chunk ^ ((r & 3) * 4 + ((r >> 2) & 3))) << 3);
-    else return r * ROW + (chunk << 3);
-  }
-  static constexpr int bytes(int rows) { return rows * ROW * 2; }
+struct RowsLayout {
+  static constexpr int ROW = D + 8;                 // elements per stored row
+  static constexpr int SLOTS_PER_ROW = ROW * 2 / 16;  // 16-byte slots incl. padding
+  __device__ __forceinline__ static int off(int r, int chunk) { return r * ROW + chunk * 8; }
+  // offset of a block shift by (r0 rows, c0 elements); r0 % 16 == 0, c0 % 8 == 0
+  static constexpr int delta(int r0, int c0) { return r0 * ROW + c0; }
+  // transposing read: offset between the two 8-row halves of a 16-row step
+  static constexpr int TR_P1 = 8 * ROW;
+  static constexpr int elems(int rows) { return rows * ROW; }
+  // chunk stored in slot `w` of row r, or -1 for padding
+  __device__ __forceinline__ static int chunk_at(int /*r*/, int w) { return w < D / 8 ? w : -1; }
 };
 
-// A/B operand whose 8 contraction elements are contiguous in an LDS row:
-// element j of lane l comes from row (row0 + l % 32), column (col0 + (l/32)*8 + j).
 template <int D>
-__device__ __forceinline__ bf16x8 lds_row_operand(const uint16_t* tile, int row0, int col0) {
+struct DualLayout : RowsLayout<D> {};
+
+template <>
+struct DualLayout<128> {
+  static constexpr int ROW = 160;  // 320-byte pitch
+  static constexpr int SLOTS_PER_ROW = 20;
+  __device__ __forceinline__ static int off(int r, int chunk) {
+    return r * ROW + (((r >> 2) & 3) + chunk) * 8;
+  }
+  static constexpr int delta(int r0, int c0) { return r0 * ROW + c0; }
+  static constexpr int TR_P1 = 8 * ROW + 16;  // +8 rows moves the shift by 2 chunks
+  static constexpr int elems(int rows) { return rows * ROW; }
+  __device__ __forceinline__ static int chunk_at(int r, int w) {
+    const int c = w - ((r >> 2) & 3);
+    return (c >= 0 && c < 16) ? c : -1;
+  }
+};
+
+// Per-lane base (elements) of a row read: row l % 32, chunk l / 32.
+template <class L>
+__device__ __forceinline__ int row_lane_base() {
   const int l = __lane_id();
-  const uint16_t* p = tile + LdsTile<D>::off(row0 + (l & 31), (col0 >> 3) + (l >> 5));
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+  return L::off(l & 31, l >> 5);
 }
 
-// A operand "X^T" for a row-major LDS tile X[row][col]: lane l gets
-//   element j = X[row0 + sigma(l/32, j)][col0 + l % 32],  j = 0..7,
-// i.e. 8 rows (in sigma order) of one column.  Two ds_read_b64_tr_b16: in each
-// group of 16 lanes, lane i addresses row (base + i/4), 4 columns starting at
-// col0 + (group % 2) * 16 + 4 * (i % 4); the instruction hands lane i the
-// element (i % 4) of the rows addressed by lanes 4e + i/4, e = 0..3.
-// row0 must be a multiple of 16 and col0 a multiple of 32.
-template <int D>
-__device__ __forceinline__ bf16x8 lds_tr_a_operand(const uint16_t* tile, int row0, int col0) {
+// Per-lane base (elements) of a transposing read: in each group of 16 lanes,
+// lane i addresses row (hh*4 + i/4) and 4 elements starting at column
+// (group % 2) * 16 + 4 * (i % 4).
+template <class L>
+__device__ __forceinline__ int tr_lane_base() {
   const int l = __lane_id();
   const int hh = l >> 5;
   const int g2 = (l >> 4) & 1;
   const int i = l & 15;
-  const int row = row0 + hh * 4 + (i >> 2);
-  const int chunk = (col0 >> 3) + g2 * 2 + ((i & 3) >> 1);
-  const int sub = (i & 1) * 4;
-  const uint16_t* p0 = tile + LdsTile<D>::off(row, chunk) + sub;
-  const uint16_t* p1 = tile + LdsTile<D>::off(row + 8, chunk) + sub;
+  return L::off(hh * 4 + (i >> 2), g2 * 2 + ((i & 3) >> 1)) + (i & 1) * 4;
+}
+
+// A/B operand whose 8 contraction elements are contiguous in an LDS row:
+// element j of lane l comes from row (row0 + l % 32), column (col0 + (l/32)*8 + j).
+// `lane` = tile + row_lane_base<L>(); row0 % 16 == 0, col0 % 8 == 0 (constants).
+template <class L>
+__device__ __forceinline__ bf16x8 lds_row_operand(const uint16_t* lane, int row0, int col0) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lane + L::delta(row0, col0)));
+}
+
+// A operand "X^T" for an LDS tile X[row][col]: lane l gets
+//   element j = X[row0 + sigma(l/32, j)][col0 + l % 32],  j = 0..7,
+// i.e. 8 rows (in sigma order) of one column, with two ds_read_b64_tr_b16
+// (the instruction hands lane i of a 16-lane group element i % 4 of the rows
+// addressed by lanes 4e + i/4, e = 0..3).  `lane` = tile + tr_lane_base<L>();
+// row0 % 16 == 0, col0 % 32 == 0 (constants).
+template <class L>
+__device__ __forceinline__ bf16x8 lds_tr_operand(const uint16_t* lane, int row0, int col0) {
+  const uint16_t* p0 = lane + L::delta(row0, col0);
+  const uint16_t* p1 = p0 + L::TR_P1;
   i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
   i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
   bf16x4 blo = __builtin_bit_cast(bf16x4, lo);
@@ -135,10 +186,65 @@ __device__ __forceinline__ bf16x8 lds_tr_a_operand(const uint16_t* tile, int row
   return out;
 }
 
-// Cooperative copy of a [rows x D] bf16 tile (rows of global stride
-// `gstride` elements) into registers: NT threads, 16 B per thread per step,
-// then into an LdsTile<D> layout.
-template <int ROWS, int D, int NT>
+// The same X^T operand, issued with inline assembly so the constant part of
+// the address goes into the instruction's offset field.  (The compiler's
+// intrinsic for this instruction neither folds offsets nor knows it cannot
+// alias in-flight direct-to-LDS copies, and so waits for them.)  The caller
+// must wait with tr_wait before using (or copying) the registers.  `lane_addr` = LDS byte
+// address of tile + tr_lane_base<L>(); ROW0 % 16 == 0, COL0 % 32 == 0.
+struct TrRegs {
+  u32x2 lo, hi;
+  __device__ __forceinline__ bf16x8 operand() const {
+    const bf16x4 blo = __builtin_bit_cast(bf16x4, lo);
+    const bf16x4 bhi = __builtin_bit_cast(bf16x4, hi);
+    bf16x8 out;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      out[j] = blo[j];
+      out[4 + j] = bhi[j];
+    }
+    return out;
+  }
+};
+
+template <class L, int ROW0, int COL0>
+__device__ __forceinline__ void tr_issue(uint32_t lane_addr, TrRegs& r) {
+  constexpr int off0 = L::delta(ROW0, COL0) * 2;
+  constexpr int off1 = off0 + L::TR_P1 * 2;
+  static_assert(off1 < 65536, "LDS offset out of range");
+  // early-clobber outputs: the second read still needs the address register
+  // after the first one has been issued (its data arrives asynchronously)
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %2 offset:%3\n\t"
+      "ds_read_b64_tr_b16 %1, %2 offset:%4"
+      : "=&v"(r.lo), "=&v"(r.hi)
+      : "v"(lane_addr), "i"(off0), "i"(off1));
+}
+
+// Wait until at most N LDS operations of this wave are outstanding; the
+// registers passed in are tied to the wait so that no use is scheduled above it.
+template <int N>
+__device__ __forceinline__ void tr_wait(TrRegs& a, TrRegs& b, TrRegs& c, TrRegs& d) {
+  asm volatile("s_waitcnt lgkmcnt(%8)"
+               : "+v"(a.lo), "+v"(a.hi), "+v"(b.lo), "+v"(b.hi), "+v"(c.lo), "+v"(c.hi),
+                 "+v"(d.lo), "+v"(d.hi)
+               : "i"(N));
+}
+template <int N>
+__device__ __forceinline__ void tr_wait(TrRegs& a, TrRegs& b) {
+  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a.lo), "+v"(a.hi), "+v"(b.lo), "+v"(b.hi) : "i"(N));
+}
+template <int N, int K>
+__device__ __forceinline__ void tr_wait(TrRegs (&r)[K]) {
+  static_assert(K == 2 || K == 4, "tr_wait handles 2 or 4 operands");
+  if constexpr (K == 4) tr_wait<N>(r[0], r[1], r[2], r[3]);
+  else tr_wait<N>(r[0], r[1]);
+}
+
+// Cooperative copy of a [ROWS x D] bf16 tile (rows of global stride `gstride`
+// elements) through registers into layout L: NT threads, 16 B per thread per
+// step.  Used where direct copies do not apply (D = 64).
+template <class L, int ROWS, int D, int NT>
 struct TileLoader {
   static constexpr int CHUNKS_PER_ROW = D / 8;
   static constexpr int TOTAL = ROWS * CHUNKS_PER_ROW;
@@ -146,22 +252,8 @@ struct TileLoader {
   static_assert(TOTAL % NT == 0, "tile must split evenly over the workgroup");
   u32x4 regs[STEPS];
 
-  // Rows >= valid_rows read as zero.
-  __device__ __forceinline__ void load(const uint16_t* base, size_t gstride, int valid_rows) {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      const int c = t + s * NT;
-      const int row = c / CHUNKS_PER_ROW;
-      const int col = (c % CHUNKS_PER_ROW) * 8;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (row < valid_rows) v = *reinterpret_cast<const u32x4*>(base + (size_t)row * gstride + col);
-      regs[s] = v;
-    }
-  }
-  // Rows >= valid_rows (valid_rows >= 1) repeat the last valid row instead of
-  // reading zeros: no branch per chunk.  Only for tiles whose out-of-range
-  // rows the caller masks out (their probabilities are exactly zero).
+  // Rows >= valid_rows (valid_rows >= 1) repeat the last valid row: callers
+  // mask them (their probabilities are exactly zero).
   __device__ __forceinline__ void load_clamped(const uint16_t* base, size_t gstride,
                                                int valid_rows) {
     const int t = threadIdx.x;
@@ -179,12 +271,66 @@ struct TileLoader {
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
       const int c = t + s * NT;
-      const int row = c / CHUNKS_PER_ROW;
-      const int chunk = c % CHUNKS_PER_ROW;
-      *reinterpret_cast<u32x4*>(lds + LdsTile<D>::off(row, chunk)) = regs[s];
+      *reinterpret_cast<u32x4*>(lds + L::off(c / CHUNKS_PER_ROW, c % CHUNKS_PER_ROW)) = regs[s];
     }
   }
 };
+
+// Direct global -> LDS copy (global_load_lds_dwordx4: no registers, no LDS
+// store instructions) of a [ROWS x 128] bf16 tile into layout L.  One
+// instruction moves 64 lanes x 16 B into 1 KB of consecutive LDS (lane l at
+// base + 16 l); lane l of instruction k therefore fills 16-byte slot 64 k + l
+// of the tile and fetches whichever global chunk the layout stores there
+// (padding slots re-read a valid chunk).  Rows >= valid_rows repeat the last
+// valid row; callers mask them.  Completion is tracked by vmcnt (wait_dma).
+template <class L, int ROWS, int NW>
+struct TileDma {
+  static constexpr int SLOTS = ROWS * L::SLOTS_PER_ROW;
+  static constexpr int INSTS = SLOTS / 64;
+  static constexpr int PER_WAVE = (INSTS + NW - 1) / NW;
+  static_assert(SLOTS % 64 == 0, "tile must fill whole 1 KB copies");
+  uint32_t goff[PER_WAVE];  // byte offset of this lane's chunk in each copy, full tiles
+  int srow[PER_WAVE];       // tile row, for clamping at a segment end
+  int schunk[PER_WAVE];
+
+  __device__ __forceinline__ void init(size_t gstride) {
+    const int l = __lane_id();
+    const int w = threadIdx.x >> 6;
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int slot = (w + NW * i) * 64 + l;
+      const int r = slot / L::SLOTS_PER_ROW;
+      int c = L::chunk_at(r, slot % L::SLOTS_PER_ROW);
+      c = c < 0 ? 0 : c;
+      srow[i] = r;
+      schunk[i] = c;
+      goff[i] = (uint32_t)(((size_t)r * gstride + (size_t)c * 8) * 2);
+    }
+  }
+  __device__ __forceinline__ void issue(const uint16_t* gbase, size_t gstride, int valid_rows,
+                                        uint16_t* lds) const {
+    const int w = threadIdx.x >> 6;
+    const bool full = valid_rows >= ROWS;
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int k = w + NW * i;
+      if (INSTS % NW != 0 && k >= INSTS) break;  // wave-uniform
+      uint32_t off = goff[i];
+      if (!full) {
+        const int rr = srow[i] < valid_rows ? srow[i] : valid_rows - 1;
+        off = (uint32_t)(((size_t)rr * gstride + (size_t)schunk[i] * 8) * 2);
+      }
+      __builtin_amdgcn_global_load_lds(
+          (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
+          (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
+    }
+  }
+};
+
+// Wait until this wave's outstanding direct-to-LDS copies (and any other
+// vector-memory loads) have landed.  A workgroup barrier after it publishes
+// the tile to every wave.
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Work schedule built by plan_kernel: items are (segment, level) pairs with
 // level j meaning "tile j of the segment" (forward / dQ) or "tile nt-1-j"

@@ -11,8 +11,8 @@
 // The probabilities are rounded to bf16 and fed back as the B operand of
 //   O^T += V^T P^T          (32 head-dim x 32 rows per MFMA tile)
 // with V^T read from the row-major LDS tile by transposing reads.  K/V tiles of
-// 64 keys are double-buffered: the global loads of tile t+1 are in flight while
-// tile t is computed.  Tiles entirely above the causal diagonal are never
+// 64 keys are staged through LDS: the global loads of tile t+1 are in flight
+// while tile t is computed.  Tiles entirely above the causal diagonal are never
 // visited; only tiles crossing the diagonal or the segment end are masked.
 //
 // Softmax statistics are kept in base 2 (log2(e) folded into the scale).  The
@@ -33,8 +33,13 @@ struct FwdCfg {
   static constexpr int BQ = 32 * NW;
   static constexpr int BK = 64;
   static constexpr int NT = NW * 64;
-  static constexpr int TILE = BK * LdsTile<D>::ROW;  // elements per LDS tile
-  static constexpr int LDS_BYTES = 2 * 2 * TILE * 2;  // {K, V} x double buffer
+  using KL = RowsLayout<D>;  // K is only read as rows
+  using VL = DualLayout<D>;  // V is only read transposed
+  static constexpr int KTILE = KL::elems(BK);
+  static constexpr int VTILE = VL::elems(BK);
+  static constexpr int KBUF = 2;  // K tiles in flight
+  static constexpr int VBUF = 3;  // V tiles in flight (ping-pong lag)
+  static constexpr int LDS_BYTES = (KBUF * KTILE + VBUF * VTILE) * 2;
 };
 
 struct FwdArgs {
@@ -55,9 +60,18 @@ struct FwdArgs {
 // key offset within a 32-key block held in accumulator register r (lane half 0)
 __device__ __forceinline__ constexpr int acc_row_off(int r) { return (r >> 2) * 8 + (r & 3); }
 
+// Ping-pong schedule: the two wave groups of the workgroup (waves 0..NW/2-1 and
+// NW/2..NW-1, one wave of each per SIMD) run the same per-tile chain
+//   S = K Q^T (matrix cores) -> softmax (VALU) -> O += V^T P^T (matrix cores)
+// half a tile apart: group 0 does the whole chain for tile t between two
+// barriers, group 1 finishes tile t-1 (softmax, PV) and then computes S for
+// tile t.  While one group is in its softmax the other keeps the matrix cores
+// busy.  V tiles are kept one step longer (three buffers) for group 1.
 template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   using C = FwdCfg<D, NW>;
+  using KL = typename C::KL;
+  using VL = typename C::VL;
   constexpr int BQ = C::BQ, BK = C::BK;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
@@ -72,6 +86,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
 
   const int l = __lane_id();
   const int w = threadIdx.x >> 6;
+  const int grp = w / (NW / 2);
   const int hh = l >> 5;
   const int row = q0 + w * 32 + (l & 31);  // this lane's query row
   const int wrow0 = q0 + w * 32;
@@ -96,99 +111,151 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   for (int i = 0; i < D / 32; ++i) oacc[i] = zero16();
   float m = -INFINITY;  // exponent offset (base-2 scaled logits)
   float lsum = 0.f;     // partial row sum over this lane's keys
+  f32x16 s[BK / 32];    // S^T of the tile in flight
 
   const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
   const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
 
-  // buffer b: K at smem + 2*b*TILE, V right after it
-  auto kbuf = [&](int b) { return smem + 2 * b * C::TILE; };
-  auto vbuf = [&](int b) { return smem + (2 * b + 1) * C::TILE; };
+  auto kbuf = [&](int t) __attribute__((always_inline)) { return smem + (t & 1) * C::KTILE; };
+  auto vbuf = [&](int t) __attribute__((always_inline)) {
+    return smem + C::KBUF * C::KTILE + (t % C::VBUF) * C::VTILE;
+  };
+  const int k_lane = row_lane_base<KL>();
+  const int v_lane = tr_lane_base<VL>();
+  auto active = [&](int t) __attribute__((always_inline)) {
+    return (wrow0 < seg_hi) && (!a.causal || seg_lo + t * BK <= wrow_last);
+  };
 
-  TileLoader<BK, D, C::NT> kl, vl;
+  // S^T for the tile's 32-key blocks; the independent chains interleave
+  auto compute_s = [&](const uint16_t* ktile) __attribute__((always_inline)) {
+    const uint16_t* kp = ktile + k_lane;
+#pragma unroll
+    for (int kb = 0; kb < BK / 32; ++kb) s[kb] = zero16();
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb)
+        s[kb] = mfma32(lds_row_operand<KL>(kp, kb * 32, ks * 16), qf[ks], s[kb]);
+  };
+
+  // mask, online softmax, then O^T += V^T P^T
+  auto softmax_pv = [&](int k0, const uint16_t* vtile) __attribute__((always_inline)) {
+    const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
+    if (need_mask) {
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb) {
+        const int lim = key_lim - (k0 + kb * 32 + hh * 4);
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (acc_row_off(r) > lim) s[kb][r] = -INFINITY;
+      }
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < BK / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
+    tmax = fmaxf(tmax, partner32(tmax));
+    const float mt = tmax * a.scale_log2;
+    const bool grow = mt > m + kRescaleSlack;
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      const float alpha = grow ? fast_exp2(m - mt) : 1.f;
+      m = grow ? mt : m;
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    const float muse = (m == -INFINITY) ? 0.f : m;
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < BK / 32; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(__builtin_fmaf(s[kb][r], a.scale_log2, -muse));
+        s[kb][r] = p;
+        psum += p;
+      }
+    lsum += psum;
+    // O^T += V^T P^T over the tile's 16-key steps; the transposing reads of
+    // step t+1 are in flight while step t multiplies
+    constexpr int NDB = D / 32, NT16 = BK / 16;
+    const uint32_t va = lds_addr(vtile) + v_lane * 2;
+    TrRegs vr[2][NDB];  // step T uses vr[T & 1]; no copies of in-flight registers
+    static_for<NDB>([&](auto DB) { tr_issue<VL, 0, DB * 32>(va, vr[0][DB]); });
+    static_for<NT16>([&](auto T) {
+      constexpr int cur = T & 1;
+      if constexpr (T + 1 < NT16) {
+        static_for<NDB>([&](auto DB) { tr_issue<VL, (T + 1) * 16, DB * 32>(va, vr[cur ^ 1][DB]); });
+        tr_wait<2 * NDB>(vr[cur]);
+      } else {
+        tr_wait<0>(vr[cur]);
+      }
+      const bf16x8 pf = pack8(s[T >> 1], (T & 1) * 8);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) oacc[db] = mfma32(vr[cur][db].operand(), pf, oacc[db]);
+    });
+  };
+
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  // rows past the segment end repeat the last key; they are always masked
-  kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-  vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-  kl.store(kbuf(0));
-  vl.store(vbuf(0));
-
-  for (int it = 0; it < ntiles; ++it) {
+  // one tile step between barriers: the two wave groups' schedules
+  auto step_compute = [&](int it) __attribute__((always_inline)) {
     const int k0 = seg_lo + it * BK;
-    const bool more = it + 1 < ntiles;
-    if (more) {
-      const int k1 = k0 + BK;
-      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+    if (grp == 0) {
+      if (active(it)) {
+        compute_s(kbuf(it));
+        softmax_pv(k0, vbuf(it));
+      }
+    } else {
+      if (it > 0 && active(it - 1)) softmax_pv(k0 - BK, vbuf(it - 1));
+      if (active(it)) compute_s(kbuf(it));
     }
-    __syncthreads();
-    const uint16_t* ks_ = kbuf(it & 1);
-    const uint16_t* vs_ = vbuf(it & 1);
-
-    const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
-    if (active) {
-      // S^T for the tile's 32-key blocks; the independent chains interleave
-      f32x16 s[BK / 32];
-#pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) s[kb] = zero16();
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks)
-#pragma unroll
-        for (int kb = 0; kb < BK / 32; ++kb)
-          s[kb] = mfma32(lds_row_operand<D>(ks_, kb * 32, ks * 16), qf[ks], s[kb]);
-
-      const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
-      if (need_mask) {
-#pragma unroll
-        for (int kb = 0; kb < BK / 32; ++kb) {
-          const int lim = key_lim - (k0 + kb * 32 + hh * 4);
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (acc_row_off(r) > lim) s[kb][r] = -INFINITY;
-        }
-      }
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
-      tmax = fmaxf(tmax, partner32(tmax));
-      const float mt = tmax * a.scale_log2;
-      const bool grow = mt > m + kRescaleSlack;
-      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
-        const float alpha = grow ? fast_exp2(m - mt) : 1.f;
-        m = grow ? mt : m;
-        lsum *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      }
-      const float muse = (m == -INFINITY) ? 0.f : m;
-      float psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(__builtin_fmaf(s[kb][r], a.scale_log2, -muse));
-          s[kb][r] = p;
-          psum += p;
-        }
-      lsum += psum;
-      // O^T += V^T P^T over the tile's 16-key steps
-#pragma unroll
-      for (int t = 0; t < BK / 16; ++t) {
-        const bf16x8 pf = pack8(s[t >> 1], (t & 1) * 8);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-          oacc[db] = mfma32(lds_tr_a_operand<D>(vs_, t * 16, db * 32), pf, oacc[db]);
-      }
+  };
+  // rows past the segment end repeat the last key; they are always masked
+  if constexpr (D == 128) {
+    // K/V tiles land in LDS by direct copies, no staging registers
+    TileDma<KL, BK, NW> kd;
+    TileDma<VL, BK, NW> vd;
+    kd.init(kvstride);
+    vd.init(kvstride);
+    auto issue = [&](int t) __attribute__((always_inline)) {
+      const int kt = seg_lo + t * BK;
+      kd.issue(kbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, kbuf(t));
+      vd.issue(vbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, vbuf(t));
+    };
+    issue(0);
+    for (int it = 0; it < ntiles; ++it) {
+      wait_dma();
+      __syncthreads();
+      if (it + 1 < ntiles) issue(it + 1);
+      step_compute(it);
     }
-    if (more) {
-      kl.store(kbuf((it + 1) & 1));
-      vl.store(vbuf((it + 1) & 1));
+  } else {
+    TileLoader<KL, BK, D, C::NT> kl;
+    TileLoader<VL, BK, D, C::NT> vl;
+    kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+    vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
+    kl.store(kbuf(0));
+    vl.store(vbuf(0));
+    for (int it = 0; it < ntiles; ++it) {
+      const bool more = it + 1 < ntiles;
+      if (more) {
+        const int k1 = seg_lo + (it + 1) * BK;
+        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+      }
+      __syncthreads();
+      step_compute(it);
+      if (more) {
+        kl.store(kbuf(it + 1));
+        vl.store(vbuf(it + 1));
+      }
     }
   }
+  if (grp == 1 && ntiles > 0 && active(ntiles - 1))
+    softmax_pv(seg_lo + (ntiles - 1) * BK, vbuf(ntiles - 1));
 
   // epilogue: normalise, write O (bf16) and LSE (natural log)
   const float ltot = lsum + partner32(lsum);
