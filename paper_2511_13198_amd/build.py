@@ -30,8 +30,8 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False, extra_flags=None) -> str:
-    tmp = LIB + ".tmp"
+def build(verbose: bool = False, extra_flags=None, out: str = LIB) -> str:
+    tmp = out + ".tmp"
     cmd = [hipcc(), *FLAGS, *(extra_flags or []), "-I", os.path.join(ROOT, "include"),
            "-o", tmp, *SOURCES]
     if verbose:
@@ -42,8 +42,8 @@ def build(verbose: bool = False, extra_flags=None) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode})")
     if verbose and res.stderr.strip():
         sys.stderr.write(res.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -241,6 +241,21 @@ __device__ __forceinline__ void tr_wait(TrRegs (&r)[K]) {
   else tr_wait<N>(r[0], r[1]);
 }
 
+// Row-read operand (see lds_row_operand) issued with inline assembly, for
+// explicitly pipelined reads; wait with row_wait before use.  `lane_addr` =
+// LDS byte address of tile + row_lane_base<L>().
+template <class L, int ROW0, int COL0>
+__device__ __forceinline__ void row_issue(uint32_t lane_addr, u32x4& r) {
+  constexpr int off = L::delta(ROW0, COL0) * 2;
+  static_assert(off < 65536, "LDS offset out of range");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(lane_addr), "i"(off));
+}
+template <int N>
+__device__ __forceinline__ void row_wait(u32x4& a, u32x4& b) {
+  asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N));
+}
+__device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& r) { return __builtin_bit_cast(bf16x8, r); }
+
 // Cooperative copy of a [ROWS x D] bf16 tile (rows of global stride `gstride`
 // elements) through registers into layout L: NT threads, 16 B per thread per
 // step.  Used where direct copies do not apply (D = 64).
@@ -331,6 +346,13 @@ struct TileDma {
 // vector-memory loads) have landed.  A workgroup barrier after it publishes
 // the tile to every wave.
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most N of this wave's vector-memory loads are outstanding
+// (loads complete in issue order, so everything older than the last N is done).
+template <int N>
+__device__ __forceinline__ void wait_dma_n() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
 
 // Work schedule built by plan_kernel: items are (segment, level) pairs with
 // level j meaning "tile j of the segment" (forward / dQ) or "tile nt-1-j"

@@ -28,6 +28,10 @@ namespace pdy {
 
 constexpr float kRescaleSlack = 8.0f;
 
+#ifndef PDY_FWD_STAGES
+#define PDY_FWD_STAGES 2
+#endif
+
 template <int D, int NW>
 struct FwdCfg {
   static constexpr int BQ = 32 * NW;
@@ -37,9 +41,10 @@ struct FwdCfg {
   using VL = DualLayout<D>;  // V is only read transposed
   static constexpr int KTILE = KL::elems(BK);
   static constexpr int VTILE = VL::elems(BK);
-  static constexpr int KBUF = 2;  // K tiles in flight
-  static constexpr int VBUF = 3;  // V tiles in flight (ping-pong lag)
-  static constexpr int LDS_BYTES = (KBUF * KTILE + VBUF * VTILE) * 2;
+  // K/V tiles in flight: direct copies run STAGES-1 tiles ahead (d = 128);
+  // the register-staged path (d = 64) double-buffers
+  static constexpr int STAGES = (D == 128) ? PDY_FWD_STAGES : 2;
+  static constexpr int LDS_BYTES = STAGES * (KTILE + VTILE) * 2;
 };
 
 struct FwdArgs {
@@ -60,13 +65,6 @@ struct FwdArgs {
 // key offset within a 32-key block held in accumulator register r (lane half 0)
 __device__ __forceinline__ constexpr int acc_row_off(int r) { return (r >> 2) * 8 + (r & 3); }
 
-// Ping-pong schedule: the two wave groups of the workgroup (waves 0..NW/2-1 and
-// NW/2..NW-1, one wave of each per SIMD) run the same per-tile chain
-//   S = K Q^T (matrix cores) -> softmax (VALU) -> O += V^T P^T (matrix cores)
-// half a tile apart: group 0 does the whole chain for tile t between two
-// barriers, group 1 finishes tile t-1 (softmax, PV) and then computes S for
-// tile t.  While one group is in its softmax the other keeps the matrix cores
-// busy.  V tiles are kept one step longer (three buffers) for group 1.
 template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   using C = FwdCfg<D, NW>;
@@ -86,7 +84,6 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
 
   const int l = __lane_id();
   const int w = threadIdx.x >> 6;
-  const int grp = w / (NW / 2);
   const int hh = l >> 5;
   const int row = q0 + w * 32 + (l & 31);  // this lane's query row
   const int wrow0 = q0 + w * 32;
@@ -116,10 +113,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
   const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
 
-  auto kbuf = [&](int t) __attribute__((always_inline)) { return smem + (t & 1) * C::KTILE; };
-  auto vbuf = [&](int t) __attribute__((always_inline)) {
-    return smem + C::KBUF * C::KTILE + (t % C::VBUF) * C::VTILE;
+  auto kbuf = [&](int t) __attribute__((always_inline)) {
+    return smem + (t % C::STAGES) * (C::KTILE + C::VTILE);
   };
+  auto vbuf = [&](int t) __attribute__((always_inline)) { return kbuf(t) + C::KTILE; };
   const int k_lane = row_lane_base<KL>();
   const int v_lane = tr_lane_base<VL>();
   auto active = [&](int t) __attribute__((always_inline)) {
@@ -127,15 +124,32 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   };
 
   // S^T for the tile's 32-key blocks; the independent chains interleave
+  // S^T for the tile's two 32-key blocks; K fragments are read PIPE k-steps
+  // ahead of the products that consume them
   auto compute_s = [&](const uint16_t* ktile) __attribute__((always_inline)) {
-    const uint16_t* kp = ktile + k_lane;
+    static_assert(BK == 64, "two 32-key blocks per tile");
+    constexpr int NKS = D / 16, PIPE = 3;
+    const uint32_t ka = lds_addr(ktile) + k_lane * 2;
+    u32x4 kr[PIPE + 1][2];
 #pragma unroll
-    for (int kb = 0; kb < BK / 32; ++kb) s[kb] = zero16();
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks)
-#pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb)
-        s[kb] = mfma32(lds_row_operand<KL>(kp, kb * 32, ks * 16), qf[ks], s[kb]);
+    for (int kb = 0; kb < 2; ++kb) s[kb] = zero16();
+    static_for<PIPE>([&](auto KS) {
+      row_issue<KL, 0, KS * 16>(ka, kr[KS][0]);
+      row_issue<KL, 32, KS * 16>(ka, kr[KS][1]);
+    });
+    static_for<NKS>([&](auto KS) {
+      constexpr int slot = KS % (PIPE + 1);
+      if constexpr (KS + PIPE < NKS) {
+        constexpr int nslot = (KS + PIPE) % (PIPE + 1);
+        row_issue<KL, 0, (KS + PIPE) * 16>(ka, kr[nslot][0]);
+        row_issue<KL, 32, (KS + PIPE) * 16>(ka, kr[nslot][1]);
+        row_wait<2 * PIPE>(kr[slot][0], kr[slot][1]);
+      } else {
+        row_wait<2 * (NKS - 1 - KS)>(kr[slot][0], kr[slot][1]);
+      }
+      s[0] = mfma32(as_bf16x8(kr[slot][0]), qf[KS], s[0]);
+      s[1] = mfma32(as_bf16x8(kr[slot][1]), qf[KS], s[1]);
+    });
   };
 
   // mask, online softmax, then O^T += V^T P^T
@@ -150,11 +164,13 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
           if (acc_row_off(r) > lim) s[kb][r] = -INFINITY;
       }
     }
-    float tmax = -INFINITY;
+    // row max over the lane's 32 logits in four independent chains
+    float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
     for (int kb = 0; kb < BK / 32; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
+      for (int r = 0; r < 16; ++r) mx[r & 3] = fmaxf(mx[r & 3], s[kb][r]);
+    float tmax = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
     tmax = fmaxf(tmax, partner32(tmax));
     const float mt = tmax * a.scale_log2;
     const bool grow = mt > m + kRescaleSlack;
@@ -168,16 +184,16 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
         for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
     }
     const float muse = (m == -INFINITY) ? 0.f : m;
-    float psum = 0.f;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < BK / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = fast_exp2(__builtin_fmaf(s[kb][r], a.scale_log2, -muse));
         s[kb][r] = p;
-        psum += p;
+        ps[r & 3] += p;
       }
-    lsum += psum;
+    lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
     // O^T += V^T P^T over the tile's 16-key steps; the transposing reads of
     // step t+1 are in flight while step t multiplies
     constexpr int NDB = D / 32, NT16 = BK / 16;
@@ -200,17 +216,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
 
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  // one tile step between barriers: the two wave groups' schedules
   auto step_compute = [&](int it) __attribute__((always_inline)) {
-    const int k0 = seg_lo + it * BK;
-    if (grp == 0) {
-      if (active(it)) {
-        compute_s(kbuf(it));
-        softmax_pv(k0, vbuf(it));
-      }
-    } else {
-      if (it > 0 && active(it - 1)) softmax_pv(k0 - BK, vbuf(it - 1));
-      if (active(it)) compute_s(kbuf(it));
+    if (active(it)) {
+      compute_s(kbuf(it));
+      softmax_pv(seg_lo + it * BK, vbuf(it));
     }
   };
   // rows past the segment end repeat the last key; they are always masked
@@ -225,11 +234,19 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
       kd.issue(kbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, kbuf(t));
       vd.issue(vbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, vbuf(t));
     };
-    issue(0);
+    constexpr int S = C::STAGES;
+    // copies this wave issues per tile (the fewest over the waves); waiting
+    // for "at most (S-2)*kMin outstanding" therefore covers tile it
+    constexpr int kMin = TileDma<KL, BK, NW>::INSTS / NW + TileDma<VL, BK, NW>::INSTS / NW;
+#pragma unroll
+    for (int t = 0; t < S - 1; ++t)
+      if (t < ntiles) issue(t);
     for (int it = 0; it < ntiles; ++it) {
-      wait_dma();
+      // tiles it+1 .. it+S-2 may still be in flight
+      if (it + S - 2 < ntiles) wait_dma_n<(S - 2) * kMin>();
+      else wait_dma();
       __syncthreads();
-      if (it + 1 < ntiles) issue(it + 1);
+      if (it + S - 1 < ntiles) issue(it + S - 1);
       step_compute(it);
     }
   } else {
@@ -254,8 +271,6 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
       }
     }
   }
-  if (grp == 1 && ntiles > 0 && active(ntiles - 1))
-    softmax_pv(seg_lo + (ntiles - 1) * BK, vbuf(ntiles - 1));
 
   // epilogue: normalise, write O (bf16) and LSE (natural log)
   const float ltot = lsum + partner32(lsum);

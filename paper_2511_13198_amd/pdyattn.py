@@ -13,7 +13,7 @@ import os
 from typing import Optional, Tuple
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpdyattn.so")
+LIB_PATH = os.environ.get("PDYATTN_LIB", os.path.join(_HERE, "libpdyattn.so"))
 
 PDY_OK = 0
 PDY_ERR_INVALID_ARG = -1
