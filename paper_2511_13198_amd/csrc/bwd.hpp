@@ -146,7 +146,11 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int nqt = (seg_hi - qstart + BQ - 1) / BQ;
   const int nsteps = nqt * g;
 
-  float stat = 0.f;  // threads 0..BQ-1: lse2 of a row; BQ..2BQ-1: D of a row
+  // threads 0..BQ-1 fetch the LSE of a row, BQ..2BQ-1 its D.  The value is
+  // only touched when stored, after the step's products, so the wait for it
+  // (which also covers the tile copies issued with it) is not on the
+  // critical path.
+  float stat = 0.f;
   auto load_stat = [&](int step) __attribute__((always_inline)) {
     const int t = threadIdx.x;
     if (t < 2 * BQ) {
@@ -154,11 +158,12 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       const int r = qstart + (step % nqt) * BQ + (t % BQ);
       const bool ok = r < seg_hi;
       const size_t idx = (size_t)h * a.total_tokens + r;
-      stat = ok ? (t < BQ ? a.lse[idx] * kLog2e : a.dd[idx]) : 0.f;
+      stat = ok ? (t < BQ ? a.lse[idx] : a.dd[idx]) : 0.f;
     }
   };
   auto store_stat = [&](int b) __attribute__((always_inline)) {
-    if (threadIdx.x < 2 * BQ) stats(b)[threadIdx.x] = stat;
+    const int t = threadIdx.x;
+    if (t < 2 * BQ) stats(b)[t] = t < BQ ? stat * kLog2e : stat;
   };
 
   const int q_row = row_lane_base<QL>();

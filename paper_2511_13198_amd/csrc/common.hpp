@@ -322,6 +322,25 @@ struct TileDma {
       goff[i] = (uint32_t)(((size_t)r * gstride + (size_t)c * 8) * 2);
     }
   }
+  // Copy I of this wave alone (I < PER_WAVE); a no-op where the wave has no
+  // copy I.  Lets a kernel spread its copies over the products of a step
+  // instead of queueing them all at once.
+  template <int I>
+  __device__ __forceinline__ void issue_one(const uint16_t* gbase, size_t gstride, int valid_rows,
+                                            uint16_t* lds) const {
+    static_assert(I < PER_WAVE, "copy index");
+    const int w = threadIdx.x >> 6;
+    const int k = w + NW * I;
+    if (INSTS % NW != 0 && k >= INSTS) return;  // wave-uniform
+    uint32_t off = goff[I];
+    if (valid_rows < ROWS) {
+      const int rr = srow[I] < valid_rows ? srow[I] : valid_rows - 1;
+      off = (uint32_t)(((size_t)rr * gstride + (size_t)schunk[I] * 8) * 2);
+    }
+    __builtin_amdgcn_global_load_lds(
+        (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
+        (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
+  }
   __device__ __forceinline__ void issue(const uint16_t* gbase, size_t gstride, int valid_rows,
                                         uint16_t* lds) const {
     const int w = threadIdx.x >> 6;

@@ -126,7 +126,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   // S^T for the tile's 32-key blocks; the independent chains interleave
   // S^T for the tile's two 32-key blocks; K fragments are read PIPE k-steps
   // ahead of the products that consume them
-  auto compute_s = [&](const uint16_t* ktile) __attribute__((always_inline)) {
+  auto compute_s = [&](const uint16_t* ktile, auto&& hook) __attribute__((always_inline)) {
     static_assert(BK == 64, "two 32-key blocks per tile");
     constexpr int NKS = D / 16, PIPE = 3;
     const uint32_t ka = lds_addr(ktile) + k_lane * 2;
@@ -149,6 +149,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
       }
       s[0] = mfma32(as_bf16x8(kr[slot][0]), qf[KS], s[0]);
       s[1] = mfma32(as_bf16x8(kr[slot][1]), qf[KS], s[1]);
+      hook(KS);
     });
   };
 
@@ -216,12 +217,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
 
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  auto step_compute = [&](int it) __attribute__((always_inline)) {
-    if (active(it)) {
-      compute_s(kbuf(it));
-      softmax_pv(seg_lo + it * BK, vbuf(it));
-    }
-  };
+  auto no_hook = [](auto) {};
   // rows past the segment end repeat the last key; they are always masked
   if constexpr (D == 128) {
     // K/V tiles land in LDS by direct copies, no staging registers
@@ -235,6 +231,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
       vd.issue(vbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, vbuf(t));
     };
     constexpr int S = C::STAGES;
+    constexpr int PK = TileDma<KL, BK, NW>::PER_WAVE, PV = TileDma<VL, BK, NW>::PER_WAVE;
     // copies this wave issues per tile (the fewest over the waves); waiting
     // for "at most (S-2)*kMin outstanding" therefore covers tile it
     constexpr int kMin = TileDma<KL, BK, NW>::INSTS / NW + TileDma<VL, BK, NW>::INSTS / NW;
@@ -246,8 +243,33 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
       if (it + S - 2 < ntiles) wait_dma_n<(S - 2) * kMin>();
       else wait_dma();
       __syncthreads();
-      if (it + S - 1 < ntiles) issue(it + S - 1);
-      step_compute(it);
+      const int tn = it + S - 1;
+      const bool more = tn < ntiles;
+      if (active(it)) {
+        // the copies of tile tn go out one per K-step of S, so that they
+        // trickle into the memory pipeline instead of queueing at once
+        const int kt = seg_lo + tn * BK;
+        const uint16_t* kg = kbase + (size_t)kt * kvstride;
+        const uint16_t* vg = vbase + (size_t)kt * kvstride;
+        uint16_t* kl = kbuf(tn);
+        uint16_t* vl = vbuf(tn);
+        auto copy = [&](auto CI) __attribute__((always_inline)) {
+          constexpr int c = decltype(CI)::value;
+          if constexpr (c < PK) {
+            if (more) kd.template issue_one<c>(kg, kvstride, seg_hi - kt, kl);
+          } else if constexpr (c < PK + PV) {
+            if (more) vd.template issue_one<c - PK>(vg, kvstride, seg_hi - kt, vl);
+          }
+        };
+        compute_s(kbuf(it), copy);
+        // copies beyond one per K-step (fewer waves per workgroup)
+        static_for<PK + PV>([&](auto CI) {
+          if constexpr (decltype(CI)::value >= D / 16) copy(CI);
+        });
+        softmax_pv(seg_lo + it * BK, vbuf(it));
+      } else if (more) {
+        issue(tn);
+      }
     }
   } else {
     TileLoader<KL, BK, D, C::NT> kl;
@@ -264,7 +286,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
         vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
       }
       __syncthreads();
-      step_compute(it);
+      if (active(it)) {
+        compute_s(kbuf(it), no_hook);
+        softmax_pv(seg_lo + it * BK, vbuf(it));
+      }
       if (more) {
         kl.store(kbuf(it + 1));
         vl.store(vbuf(it + 1));
