@@ -50,6 +50,13 @@ __global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict
   }
 }
 
+#ifndef PDY_DQ_BK
+#define PDY_DQ_BK 128
+#endif
+#ifndef PDY_DKDV_PIPE
+#define PDY_DKDV_PIPE 2
+#endif
+
 struct BwdArgs {
   const uint16_t* q;
   const uint16_t* k;
@@ -169,8 +176,6 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int q_row = row_lane_base<QL>();
   const int q_tr = tr_lane_base<QL>();
   const int k_row = row_lane_base<KL>();
-  const uint16_t* const kp = ktile_s + k_row;
-  const uint16_t* const vp = vtile + k_row;
 
   auto compute = [&](int step) __attribute__((always_inline)) {
     const int b = step & 1;
@@ -182,14 +187,35 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     const bool active = (kw0 < seg_hi) && (wr0 < seg_hi) && (!a.causal || wr0 + 31 >= kw0);
     if (!active) return;
     const bool need_mask = (a.causal && wr0 < kw0 + 31) || (wr0 + 32 > seg_hi);
-    // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows
+    // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows;
+    // the four operand fragments of a K-step are read PIPE steps ahead
     f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      s = mfma32(lds_row_operand<QL>(qs + q_row, half * 32, ks * 16),
-                 lds_row_operand<KL>(kp, pw * 32, ks * 16), s);
-      dp = mfma32(lds_row_operand<QL>(gs + q_row, half * 32, ks * 16),
-                  lds_row_operand<KL>(vp, pw * 32, ks * 16), dp);
+    {
+      constexpr int NKS = D / 16, PIPE = PDY_DKDV_PIPE;
+      const uint32_t qa = lds_addr(qs) + (q_row + half * 32 * QL::ROW) * 2;
+      const uint32_t ga = lds_addr(gs) + (q_row + half * 32 * QL::ROW) * 2;
+      const uint32_t ka = lds_addr(ktile_s) + (k_row + pw * 32 * KL::ROW) * 2;
+      const uint32_t va = lds_addr(vtile) + (k_row + pw * 32 * KL::ROW) * 2;
+      u32x4 rq[PIPE + 1], rk[PIPE + 1], rg[PIPE + 1], rv[PIPE + 1];
+      auto rd = [&](auto KS) __attribute__((always_inline)) {
+        constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
+        row_issue<QL, 0, ks * 16>(qa, rq[sl]);
+        row_issue<KL, 0, ks * 16>(ka, rk[sl]);
+        row_issue<QL, 0, ks * 16>(ga, rg[sl]);
+        row_issue<KL, 0, ks * 16>(va, rv[sl]);
+      };
+      static_for<PIPE>([&](auto KS) { rd(KS); });
+      static_for<NKS>([&](auto KS) {
+        constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
+        if constexpr (ks + PIPE < NKS) {
+          rd(std::integral_constant<int, ks + PIPE>{});
+          row_wait<4 * PIPE>(rq[sl], rk[sl], rg[sl], rv[sl]);
+        } else {
+          row_wait<4 * (NKS - 1 - ks)>(rq[sl], rk[sl], rg[sl], rv[sl]);
+        }
+        s = mfma32(as_bf16x8(rq[sl]), as_bf16x8(rk[sl]), s);
+        dp = mfma32(as_bf16x8(rg[sl]), as_bf16x8(rv[sl]), dp);
+      });
     }
     if (need_mask) {  // diagonal or segment-end step only
       // causal: key visible to row iff row - (wr0 + hh*4) >= key - (wr0 + hh*4)
@@ -350,7 +376,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
 template <int D, int NW>
 struct DqCfg {
   static constexpr int BQ = 32 * NW;
-  static constexpr int BK = 64;
+  static constexpr int BK = (D == 128) ? PDY_DQ_BK : 64;  // keys per tile
   static constexpr int NT = NW * 64;
   using KL = DualLayout<D>;  // K is read as rows (S^T) and transposed (dQ^T)
   using VL = RowsLayout<D>;  // V is read as rows (dP^T)
@@ -422,18 +448,35 @@ __global__ void __launch_bounds__(NW * 64) bwd_dq_kernel(BwdArgs a) {
     const int k0 = seg_lo + it * BK;
     const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
     if (!active) return;
-    const uint16_t* kp = kbuf(it) + k_row;
+    const uint32_t kra = lds_addr(kbuf(it)) + k_row * 2;
     const uint32_t ka = lds_addr(kbuf(it)) + k_tr * 2;
-    const uint16_t* vp = vbuf(it) + v_row;
+    const uint32_t vra = lds_addr(vbuf(it)) + v_row * 2;
     const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
     // one 32-key block at a time keeps S^T and dP^T to 32 registers
-#pragma unroll
-    for (int kb = 0; kb < BK / 32; ++kb) {
+    static_for<BK / 32>([&](auto KB) {
+      constexpr int kb = decltype(KB)::value;
+      // S^T and dP^T; the K and V fragments are read PIPE K-steps ahead
       f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        s = mfma32(lds_row_operand<KL>(kp, kb * 32, ks * 16), qf[ks], s);
-        dp = mfma32(lds_row_operand<VL>(vp, kb * 32, ks * 16), gf[ks], dp);
+      {
+        constexpr int NKS = D / 16, PIPE = 2;
+        u32x4 rk[PIPE + 1], rv[PIPE + 1];
+        auto rd = [&](auto KS) __attribute__((always_inline)) {
+          constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
+          row_issue<KL, kb * 32, ks * 16>(kra, rk[sl]);
+          row_issue<VL, kb * 32, ks * 16>(vra, rv[sl]);
+        };
+        static_for<PIPE>([&](auto KS) { rd(KS); });
+        static_for<NKS>([&](auto KS) {
+          constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
+          if constexpr (ks + PIPE < NKS) {
+            rd(std::integral_constant<int, ks + PIPE>{});
+            row_wait<2 * PIPE>(rk[sl], rv[sl]);
+          } else {
+            row_wait<2 * (NKS - 1 - ks)>(rk[sl], rv[sl]);
+          }
+          s = mfma32(as_bf16x8(rk[sl]), qf[ks], s);
+          dp = mfma32(as_bf16x8(rv[sl]), gf[ks], dp);
+        });
       }
       if (need_mask) {  // diagonal or segment-end tile only
         const int lim = key_lim - (k0 + kb * 32 + hh * 4);
@@ -462,7 +505,7 @@ __global__ void __launch_bounds__(NW * 64) bwd_dq_kernel(BwdArgs a) {
       const bf16x8 sb1 = pack8(s, 8);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) dqa[db] = mfma32(kt1[db].operand(), sb1, dqa[db]);
-    }
+    });
   };
 
   // rows past the segment end repeat the last key; they are always masked

@@ -254,6 +254,10 @@ template <int N>
 __device__ __forceinline__ void row_wait(u32x4& a, u32x4& b) {
   asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N));
 }
+template <int N>
+__device__ __forceinline__ void row_wait(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
+  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "i"(N));
+}
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& r) { return __builtin_bit_cast(bf16x8, r); }
 
 // Cooperative copy of a [ROWS x D] bf16 tile (rows of global stride `gstride`

@@ -28,6 +28,9 @@ namespace pdy {
 
 constexpr float kRescaleSlack = 8.0f;
 
+#ifndef PDY_FWD_BK
+#define PDY_FWD_BK 128
+#endif
 #ifndef PDY_FWD_STAGES
 #define PDY_FWD_STAGES 2
 #endif
@@ -35,7 +38,8 @@ constexpr float kRescaleSlack = 8.0f;
 template <int D, int NW>
 struct FwdCfg {
   static constexpr int BQ = 32 * NW;
-  static constexpr int BK = 64;
+  static constexpr int BK = (D == 128) ? PDY_FWD_BK : 64;  // keys per tile (one barrier)
+  static constexpr int BKS = 64;                            // keys per softmax step
   static constexpr int NT = NW * 64;
   using KL = RowsLayout<D>;  // K is only read as rows
   using VL = DualLayout<D>;  // V is only read transposed
@@ -70,7 +74,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   using C = FwdCfg<D, NW>;
   using KL = typename C::KL;
   using VL = typename C::VL;
-  constexpr int BQ = C::BQ, BK = C::BK;
+  constexpr int BQ = C::BQ, BK = C::BK, BKS = C::BKS;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   const int item = blockIdx.x / a.hq;
@@ -108,7 +112,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   for (int i = 0; i < D / 32; ++i) oacc[i] = zero16();
   float m = -INFINITY;  // exponent offset (base-2 scaled logits)
   float lsum = 0.f;     // partial row sum over this lane's keys
-  f32x16 s[BK / 32];    // S^T of the tile in flight
+  f32x16 s[BKS / 32];   // S^T of the keys in flight
 
   const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
   const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
@@ -127,38 +131,45 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
   // S^T for the tile's two 32-key blocks; K fragments are read PIPE k-steps
   // ahead of the products that consume them
   auto compute_s = [&](const uint16_t* ktile, auto&& hook) __attribute__((always_inline)) {
-    static_assert(BK == 64, "two 32-key blocks per tile");
-    constexpr int NKS = D / 16, PIPE = 3;
+    constexpr int NKS = D / 16, NKB = BKS / 32;
+    static_assert(NKB == 2 || NKB == 4, "two or four 32-key blocks per tile");
+    constexpr int PIPE = NKB == 2 ? 3 : 1;  // lgkmcnt counts at most 15 reads
     const uint32_t ka = lds_addr(ktile) + k_lane * 2;
-    u32x4 kr[PIPE + 1][2];
+    u32x4 kr[PIPE + 1][NKB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) s[kb] = zero16();
-    static_for<PIPE>([&](auto KS) {
-      row_issue<KL, 0, KS * 16>(ka, kr[KS][0]);
-      row_issue<KL, 32, KS * 16>(ka, kr[KS][1]);
-    });
+    for (int kb = 0; kb < NKB; ++kb) s[kb] = zero16();
+    auto rd = [&](auto KS) __attribute__((always_inline)) {
+      constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
+      static_for<NKB>([&](auto KB) {
+        row_issue<KL, decltype(KB)::value * 32, ks * 16>(ka, kr[sl][KB]);
+      });
+    };
+    auto wt = [&](auto KS, auto N) __attribute__((always_inline)) {
+      constexpr int sl = decltype(KS)::value % (PIPE + 1);
+      if constexpr (NKB == 2) row_wait<decltype(N)::value>(kr[sl][0], kr[sl][1]);
+      else row_wait<decltype(N)::value>(kr[sl][0], kr[sl][1], kr[sl][2], kr[sl][3]);
+    };
+    static_for<PIPE>([&](auto KS) { rd(KS); });
     static_for<NKS>([&](auto KS) {
-      constexpr int slot = KS % (PIPE + 1);
-      if constexpr (KS + PIPE < NKS) {
-        constexpr int nslot = (KS + PIPE) % (PIPE + 1);
-        row_issue<KL, 0, (KS + PIPE) * 16>(ka, kr[nslot][0]);
-        row_issue<KL, 32, (KS + PIPE) * 16>(ka, kr[nslot][1]);
-        row_wait<2 * PIPE>(kr[slot][0], kr[slot][1]);
+      constexpr int ks = decltype(KS)::value, slot = ks % (PIPE + 1);
+      if constexpr (ks + PIPE < NKS) {
+        rd(std::integral_constant<int, ks + PIPE>{});
+        wt(KS, std::integral_constant<int, NKB * PIPE>{});
       } else {
-        row_wait<2 * (NKS - 1 - KS)>(kr[slot][0], kr[slot][1]);
+        wt(KS, std::integral_constant<int, NKB * (NKS - 1 - ks)>{});
       }
-      s[0] = mfma32(as_bf16x8(kr[slot][0]), qf[KS], s[0]);
-      s[1] = mfma32(as_bf16x8(kr[slot][1]), qf[KS], s[1]);
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) s[kb] = mfma32(as_bf16x8(kr[slot][kb]), qf[ks], s[kb]);
       hook(KS);
     });
   };
 
   // mask, online softmax, then O^T += V^T P^T
   auto softmax_pv = [&](int k0, const uint16_t* vtile) __attribute__((always_inline)) {
-    const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
+    const bool need_mask = (a.causal && k0 + BKS - 1 > wrow0) || (k0 + BKS > seg_hi);
     if (need_mask) {
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) {
+      for (int kb = 0; kb < BKS / 32; ++kb) {
         const int lim = key_lim - (k0 + kb * 32 + hh * 4);
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -168,7 +179,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
     // row max over the lane's 32 logits in four independent chains
     float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
-    for (int kb = 0; kb < BK / 32; ++kb)
+    for (int kb = 0; kb < BKS / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx[r & 3] = fmaxf(mx[r & 3], s[kb][r]);
     float tmax = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
@@ -187,7 +198,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
     const float muse = (m == -INFINITY) ? 0.f : m;
     float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < BK / 32; ++kb)
+    for (int kb = 0; kb < BKS / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = fast_exp2(__builtin_fmaf(s[kb][r], a.scale_log2, -muse));
@@ -197,7 +208,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
     lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
     // O^T += V^T P^T over the tile's 16-key steps; the transposing reads of
     // step t+1 are in flight while step t multiplies
-    constexpr int NDB = D / 32, NT16 = BK / 16;
+    constexpr int NDB = D / 32, NT16 = BKS / 16;
     const uint32_t va = lds_addr(vtile) + v_lane * 2;
     TrRegs vr[2][NDB];  // step T uses vr[T & 1]; no copies of in-flight registers
     static_for<NDB>([&](auto DB) { tr_issue<VL, 0, DB * 32>(va, vr[0][DB]); });
@@ -261,12 +272,24 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
             if (more) vd.template issue_one<c - PK>(vg, kvstride, seg_hi - kt, vl);
           }
         };
-        compute_s(kbuf(it), copy);
-        // copies beyond one per K-step (fewer waves per workgroup)
-        static_for<PK + PV>([&](auto CI) {
-          if constexpr (decltype(CI)::value >= D / 16) copy(CI);
+        // the tile is taken in softmax steps of BKS keys; the first step
+        // issues the copies
+        static_for<BK / BKS>([&](auto SUB) {
+          constexpr int sub = decltype(SUB)::value;
+          const int k0s = seg_lo + it * BK + sub * BKS;
+          if (sub == 0 || (k0s < kv_end && (!a.causal || k0s <= wrow_last))) {
+            compute_s(kbuf(it) + sub * BKS * KL::ROW, [&](auto KS) __attribute__((always_inline)) {
+              if constexpr (sub == 0) copy(KS);
+            });
+            softmax_pv(k0s, vbuf(it) + sub * BKS * VL::ROW);
+          }
+          if constexpr (sub == 0) {
+            // copies beyond one per K-step
+            static_for<PK + PV>([&](auto CI) {
+              if constexpr (decltype(CI)::value >= D / 16) copy(CI);
+            });
+          }
         });
-        softmax_pv(seg_lo + it * BK, vbuf(it));
       } else if (more) {
         issue(tn);
       }
