@@ -88,6 +88,25 @@ def cpu_baseline(w, inputs, sample_tokens: int):
     }
 
 
+def recorded_traffic(workload_name: str, kernel: str):
+    """HBM bytes per launch of `kernel` (FETCH_SIZE + WRITE_SIZE, each scaled
+    by a plain-copy calibration) from the committed rocprofv3 summary of this
+    workload, or None when there is none or the kernel sources changed since
+    the counters were taken."""
+    from paper_2511_13198_amd import profiling
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                        f"{workload_name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_sha256") != profiling.source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel, {})
+    if "fetch_bytes" not in k or "write_bytes" not in k:
+        return None
+    return k["fetch_bytes"] + k["write_bytes"]
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -162,7 +181,7 @@ def main():
         "peak": acc.PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(achieved / acc.PEAK_BF16_TFLOPS, 4),
-        "traffic": None,
+        "traffic": recorded_traffic(w.name, dom),
     }
     print(f"[bench] {ms:.3f} ms/step, {value:.1f} TFLOP/s; kernels (avg ms): "
           + ", ".join(f"{kk}={vv:.3f}" for kk, vv in kernels_ms.items()),
