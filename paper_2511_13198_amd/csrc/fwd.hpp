@@ -38,7 +38,9 @@ constexpr float kRescaleSlack = 8.0f;
 template <int D, int NW>
 struct FwdCfg {
   static constexpr int BQ = 32 * NW;
-  static constexpr int BK = (D == 128) ? PDY_FWD_BK : 64;  // keys per tile (one barrier)
+  // keys per tile (one barrier); 4-wave workgroups keep 64 so that two of
+  // them fit a CU's LDS
+  static constexpr int BK = (D == 128 && NW == 8) ? PDY_FWD_BK : 64;
   static constexpr int BKS = 64;                            // keys per softmax step
   static constexpr int NT = NW * 64;
   using KL = RowsLayout<D>;  // K is only read as rows
@@ -70,7 +72,7 @@ struct FwdArgs {
 __device__ __forceinline__ constexpr int acc_row_off(int r) { return (r >> 2) * 8 + (r & 3); }
 
 template <int D, int NW>
-__global__ void __launch_bounds__(NW * 64) fwd_kernel(FwdArgs a) {
+__global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a) {
   using C = FwdCfg<D, NW>;
   using KL = typename C::KL;
   using VL = typename C::VL;

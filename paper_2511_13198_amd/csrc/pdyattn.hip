@@ -45,7 +45,10 @@ int tiles_of(const Sizes& s, int tile) {
 }
 
 // forward workgroup size: 8 waves (256 query rows) unless segments are short
-int fwd_waves(const Sizes& s) { return s.maxlen > 128 ? 8 : 4; }
+#ifndef PDY_WAVES_LONG
+#define PDY_WAVES_LONG 8
+#endif
+int fwd_waves(const Sizes& s) { return s.maxlen > 128 ? PDY_WAVES_LONG : 4; }
 
 pdy_status check_sizes(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv, int32_t d,
                        Sizes* out) {

@@ -50,6 +50,8 @@ def _full_parity(lengths, hq, hkv, d, causal, scale=None, seed=wl.SEED):
     ([300, 65, 1], 4, 4, 128, False, None),
     ([2048, 33], 8, 2, 128, True, None),
     ([1], 1, 1, 64, True, None),                            # single token
+    ([128, 1, 100, 37, 128], 4, 2, 128, True, None),        # every segment <= 128: 4-wave kernels
+    ([96, 3, 128], 2, 2, 128, False, None),                 # same, non-causal
 ])
 def test_full_parity_small(lengths, hq, hkv, d, causal, scale):
     _full_parity(lengths, hq, hkv, d, causal, scale)
