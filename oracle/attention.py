@@ -225,3 +225,86 @@ def _head(x, h):
     if hasattr(x, "head"):
         return x.head(h)
     return np.asarray(x[:, h], dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Chunked (context-parallel) attention of one long sequence.
+#
+# Sequence sharding (the context-parallel strategies of section 2.2) gives a
+# device the queries at absolute positions q_offset .. q_offset+Tq-1 and,
+# one chunk at a time, the keys/values at k_offset .. k_offset+Tk-1.  Eq. (2)
+# restricted to one key chunk yields a partial output and its log-sum-exp;
+# the full result is their log-sum-exp weighted combination.  Readings: the
+# causal rule compares absolute positions (key visible iff its position <=
+# the query's); a row that sees no key of a chunk gets O = 0 and LSE = -inf
+# (the neutral element of the combination).
+# ---------------------------------------------------------------------------
+def _chunk_logits(qh, kh, q_offset: int, k_offset: int, causal: bool, scale: float):
+    s = scale * (qh @ kh.T)
+    if causal:
+        qpos = q_offset + np.arange(qh.shape[0])[:, None]
+        kpos = k_offset + np.arange(kh.shape[0])[None, :]
+        s = np.where(kpos <= qpos, s, -np.inf)
+    return s
+
+
+def partial_forward(q, k, v, q_offset: int, k_offset: int, causal: bool, scale: float):
+    """O_c [Tq, Hq, d] and LSE_c [Hq, Tq] of a query chunk over one key/value
+    chunk of the same sequence."""
+    Tq, Hq, _ = q.shape
+    Hkv = k.shape[1]
+    g = Hq // Hkv
+    o = np.zeros((Tq, Hq, v.shape[2]))
+    lse = np.full((Hq, Tq), -np.inf)
+    for h in range(Hq):
+        hk = h // g
+        s = _chunk_logits(q[:, h], k[:, hk], q_offset, k_offset, causal, scale)
+        seen = np.isfinite(s).any(axis=1)
+        if not seen.any():
+            continue
+        l, p = _softmax_stats(s[seen])
+        lse[h, seen] = l
+        o[seen, h] = p @ v[:, hk]
+    return o, lse
+
+
+def merge(parts):
+    """Combine partial (O_c, LSE_c) pairs of the same query rows:
+    LSE = log sum_c exp(LSE_c),  O = sum_c exp(LSE_c - LSE) O_c."""
+    lses = np.stack([l for _, l in parts])           # [C, Hq, Tq]
+    top = np.max(lses, axis=0)
+    safe = np.where(np.isfinite(top), top, 0.0)
+    w = np.exp(lses - safe[None])                    # exp(-inf) = 0
+    tot = np.sum(w, axis=0)
+    lse = np.where(tot > 0, safe + np.log(np.where(tot > 0, tot, 1.0)), -np.inf)
+    o = np.zeros_like(parts[0][0])
+    for (oc, _), wc in zip(parts, w):
+        coef = np.where(tot > 0, wc / np.where(tot > 0, tot, 1.0), 0.0)  # [Hq, Tq]
+        o += oc * coef.T[:, :, None]
+    return o, lse
+
+
+def partial_backward(q, k, v, o, lse, do, q_offset: int, k_offset: int, causal: bool,
+                     scale: float):
+    """Contribution of one (query chunk, key chunk) pair to the gradient of
+    L = sum(dO * O), given the final O and LSE of the query rows (over all
+    key chunks).  Returns (dQ_c [Tq, Hq, d], dK_c, dV_c [Tk, Hkv, d]); dQ of the
+    query chunk is the sum over key chunks, dK/dV of a key chunk the sum over
+    query chunks."""
+    Tq, Hq, _ = q.shape
+    Hkv = k.shape[1]
+    g = Hq // Hkv
+    dq = np.zeros_like(q, dtype=np.float64)
+    dk = np.zeros_like(k, dtype=np.float64)
+    dv = np.zeros_like(v, dtype=np.float64)
+    for h in range(Hq):
+        hk = h // g
+        s = _chunk_logits(q[:, h], k[:, hk], q_offset, k_offset, causal, scale)
+        l = lse[h][:, None]
+        p = np.where(np.isfinite(l), np.exp(s - np.where(np.isfinite(l), l, 0.0)), 0.0)
+        D = np.sum(do[:, h] * o[:, h], axis=1)
+        ds = p * (do[:, h] @ v[:, hk].T - D[:, None])
+        dq[:, h] = scale * (ds @ k[:, hk])
+        dk[:, hk] += scale * (ds.T @ q[:, h])
+        dv[:, hk] += p.T @ do[:, h]
+    return dq, dk, dv
