@@ -91,6 +91,56 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
                     float* dq, float* dk, float* dv,
                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- One long sequence split into chunks (context parallelism) ----
+ * Sequence-sharded strategies (section 2.2: Megatron-style context
+ * parallelism, its ZeRO-3 variant, the fine-grained two-level ring) give a
+ * device the queries of positions q_offset .. q_offset+tq-1 and, one chunk
+ * at a time, the keys/values of positions k_offset .. k_offset+tk-1 of the
+ * same sequence.  Eq. (2) restricted to one key chunk gives a partial output
+ * and log-sum-exp; attn_merge combines partials of the same rows into the
+ * result over the union of the chunks.  With causal = 1 a key is visible to
+ * a query iff its position is <= the query's; a row that sees no key of the
+ * chunk gets o = 0 and lse = -inf (the neutral element of attn_merge).
+ * Sizes: tq, tk >= 0, offsets >= 0; tensors [tq, Hq, d] (q, o, dout, dq),
+ * [tk, Hkv, d] (k, v, dk, dv), lse fp32 [Hq, tq].  Other rules as above. */
+size_t attn_fwd_chunk_workspace_size(int32_t tq, int32_t tk, int32_t num_heads_q,
+                                     int32_t num_heads_kv, int32_t head_dim);
+size_t attn_bwd_chunk_workspace_size(int32_t tq, int32_t tk, int32_t num_heads_q,
+                                     int32_t num_heads_kv, int32_t head_dim);
+
+/* Partial forward of a query chunk over one key/value chunk:
+ * o bf16 [tq, Hq, d] and lse fp32 [Hq, tq] (out).  tq = 0 is a no-op;
+ * tk = 0 gives o = 0, lse = -inf (k and v may then be NULL). */
+pdy_status attn_fwd_chunk(const void* q, const void* k, const void* v, int32_t tq, int32_t tk,
+                          int32_t q_offset, int32_t k_offset,
+                          int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                          int32_t causal, float scale,
+                          void* o, float* lse,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Contribution of one (query chunk, key chunk) pair to the gradient of
+ * sum(dout * O): o and lse are the FINAL output and log-sum-exp of the query
+ * rows (merged over every key chunk), dout their upstream gradient.
+ * Writes dq fp32 [tq, Hq, d] (this pair's part; the chunk's dQ is the sum
+ * over its key chunks) and dk, dv fp32 [tk, Hkv, d] (this pair's part; a key
+ * chunk's gradient is the sum over query chunks).  Rows with lse = -inf
+ * contribute nothing.  tq = 0 writes zero dk, dv. */
+pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const void* o,
+                          const float* lse, const void* dout, int32_t tq, int32_t tk,
+                          int32_t q_offset, int32_t k_offset,
+                          int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                          int32_t causal, float scale,
+                          float* dq, float* dk, float* dv,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Combine two partial results of the same T query rows:
+ *   lse = log(exp(lse_a) + exp(lse_b)),  o = sum_x exp(lse_x - lse) o_x
+ * (bf16 [T, Hq, d] and fp32 [Hq, T]).  o/lse may alias o_a/lse_a or
+ * o_b/lse_b (in place).  Needs no workspace. */
+pdy_status attn_merge(const void* o_a, const float* lse_a, const void* o_b, const float* lse_b,
+                      int32_t total_tokens, int32_t num_heads_q, int32_t head_dim,
+                      void* o, float* lse, void* stream);
+
 /* Debug helper: copies cu_seqlens to the host (synchronising `stream`) and
  * checks cu[0] = 0, monotonicity and cu[num_seqs] = total_tokens.  On success
  * writes the longest segment length to *max_seqlen_out (may be NULL). */

@@ -76,6 +76,13 @@ struct BwdArgs {
   int causal;
   float scale;
   float scale_log2;
+  // chunk mode (chunked != 0): one query chunk of total_tokens rows against
+  // one key/value chunk of tk rows of the same sequence; key j is visible to
+  // row i (causal) iff j <= i + shift.  Otherwise rows and keys share the
+  // packed segments of cu.
+  int chunked;
+  int tk;
+  int shift;
 };
 
 // dK/dV: one workgroup of 8 waves per (segment, kv head, 128-key tile).  Waves
@@ -113,11 +120,16 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int hk = blockIdx.x % a.hkv;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
-  const int seg_lo = a.cu[seg];
-  const int seg_hi = a.cu[seg + 1];
-  const int nt = (seg_hi - seg_lo + BK - 1) / BK;
+  // keys [k_lo, k_hi) (this workgroup: a tile of them), query rows
+  // [q_lo, q_hi); causal: key j visible to row i iff j <= i + shift
+  const int k_lo = a.chunked ? 0 : a.cu[seg];
+  const int k_hi = a.chunked ? a.tk : a.cu[seg + 1];
+  const int q_lo = a.chunked ? 0 : k_lo;
+  const int q_hi = a.chunked ? a.total_tokens : k_hi;
+  const int shift = a.chunked ? a.shift : 0;
+  const int nt = (k_hi - k_lo + BK - 1) / BK;
   const int ktile = nt - 1 - level;
-  const int k0 = seg_lo + ktile * BK;
+  const int k0 = k_lo + ktile * BK;
   const int g = a.hq / a.hkv;
 
   const int l = __lane_id();
@@ -149,8 +161,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   };
 
   // query rows that can see this key tile
-  const int qstart = a.causal ? k0 : seg_lo;
-  const int nqt = (seg_hi - qstart + BQ - 1) / BQ;
+  const int qstart = a.causal ? max(q_lo, k0 - shift) : q_lo;
+  const int nqt = max(0, (q_hi - qstart + BQ - 1) / BQ);
   const int nsteps = nqt * g;
 
   // threads 0..BQ-1 fetch the LSE of a row, BQ..2BQ-1 its D.  The value is
@@ -163,14 +175,16 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     if (t < 2 * BQ) {
       const int h = hk * g + step / nqt;
       const int r = qstart + (step % nqt) * BQ + (t % BQ);
-      const bool ok = r < seg_hi;
+      const bool ok = r < q_hi;
       const size_t idx = (size_t)h * a.total_tokens + r;
       stat = ok ? (t < BQ ? a.lse[idx] : a.dd[idx]) : 0.f;
     }
   };
   auto store_stat = [&](int b) __attribute__((always_inline)) {
     const int t = threadIdx.x;
-    if (t < 2 * BQ) stats(b)[t] = t < BQ ? stat * kLog2e : stat;
+    // a row without any visible key (LSE = -inf) must contribute nothing:
+    // +inf makes exp2(s * scale - lse2) vanish for every s
+    if (t < 2 * BQ) stats(b)[t] = t < BQ ? (stat == -INFINITY ? INFINITY : stat * kLog2e) : stat;
   };
 
   const int q_row = row_lane_base<QL>();
@@ -184,9 +198,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     const float* lse_s = stats(b);
     const float* dd_s = lse_s + BQ;
     const int wr0 = qstart + (step % nqt) * BQ + half * 32;  // first row of this wave
-    const bool active = (kw0 < seg_hi) && (wr0 < seg_hi) && (!a.causal || wr0 + 31 >= kw0);
+    const bool active = (kw0 < k_hi) && (wr0 < q_hi) && (!a.causal || wr0 + 31 + shift >= kw0);
     if (!active) return;
-    const bool need_mask = (a.causal && wr0 < kw0 + 31) || (wr0 + 32 > seg_hi);
+    const bool need_mask = (a.causal && wr0 + shift < kw0 + 31) || (wr0 + 32 > q_hi);
     // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows;
     // the four operand fragments of a K-step are read PIPE steps ahead
     f32x16 s = zero16(), dp = zero16();
@@ -218,9 +232,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       });
     }
     if (need_mask) {  // diagonal or segment-end step only
-      // causal: key visible to row iff row - (wr0 + hh*4) >= key - (wr0 + hh*4)
-      const int rel = a.causal ? key - wr0 - hh * 4 : -32;
-      const int rows_left = seg_hi - wr0 - hh * 4;
+      // causal: key visible to row iff row - (wr0 + hh*4) >= key - shift - (wr0 + hh*4)
+      const int rel = a.causal ? key - shift - wr0 - hh * 4 : -32;
+      const int rows_left = q_hi - wr0 - hh * 4;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int off = acc_row_off(r);
@@ -272,7 +286,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     return t + (size_t)r0 * qstride + (size_t)h * D;
   };
   auto rows_valid = [&](int step) __attribute__((always_inline)) {
-    return seg_hi - (qstart + (step % nqt) * BQ);
+    return q_hi - (qstart + (step % nqt) * BQ);
   };
 
   // K and V tiles (keys past the segment end repeat the last key; their
@@ -282,8 +296,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     {
       TileDma<KL, BK, NW> kvd;
       kvd.init(kvstride);
-      kvd.issue(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0, ktile_s);
-      kvd.issue(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0, vtile);
+      kvd.issue(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, ktile_s);
+      kvd.issue(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, vtile);
     }
     TileDma<QL, BQ, NW> qd;
     qd.init(qstride);
@@ -310,8 +324,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   } else {
     {
       TileLoader<KL, BK, D, C::NT> kl, vl;
-      kl.load_clamped(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
-      vl.load_clamped(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, seg_hi - k0);
+      kl.load_clamped(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0);
+      vl.load_clamped(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0);
       kl.store(ktile_s);
       vl.store(vtile);
     }
@@ -352,7 +366,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       }
   }
   __syncthreads();
-  if (half == 0 && key < seg_hi) {
+  if (half == 0 && key < k_hi) {
     float* dkp = a.dk + (size_t)key * kvstride + (size_t)hk * D;
     float* dvp = a.dv + (size_t)key * kvstride + (size_t)hk * D;
 #pragma unroll
@@ -397,8 +411,13 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const int h = blockIdx.x % a.hq;
   int seg, level;
   if (!plan_lookup(a.plan_q, item, seg, level)) return;
-  const int seg_lo = a.cu[seg];
-  const int seg_hi = a.cu[seg + 1];
+  // query rows [seg_lo, seg_hi), keys [k_lo, k_hi); causal: key j visible to
+  // row i iff j <= i + shift
+  const int seg_lo = a.chunked ? 0 : a.cu[seg];
+  const int seg_hi = a.chunked ? a.total_tokens : a.cu[seg + 1];
+  const int k_lo = a.chunked ? 0 : seg_lo;
+  const int k_hi = a.chunked ? a.tk : seg_hi;
+  const int shift = a.chunked ? a.shift : 0;
   const int q0 = seg_lo + level * BQ;
   const int hk = h / (a.hq / a.hkv);
 
@@ -408,7 +427,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const int row = q0 + w * 32 + (l & 31);
   const int wrow0 = q0 + w * 32;
   const int wrow_last = wrow0 + 31;
-  const int key_lim = a.causal ? min(row, seg_hi - 1) : seg_hi - 1;
+  const int key_lim = a.causal ? min(row + shift, k_hi - 1) : k_hi - 1;
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
 
@@ -426,14 +445,16 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
     if (ok) {
       lse2 = a.lse[(size_t)h * a.total_tokens + row] * kLog2e;
       ddv = a.dd[(size_t)h * a.total_tokens + row];
+      // a row without any visible key has LSE = -inf and no gradient
+      if (lse2 == -INFINITY) lse2 = INFINITY;
     }
   }
   f32x16 dqa[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) dqa[i] = zero16();
 
-  const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
-  const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
+  const int kv_end = a.causal ? min(k_hi, q0 + BQ + shift) : k_hi;
+  const int ntiles = max(0, (kv_end - k_lo + BK - 1) / BK);
   auto kbuf = [&](int t) __attribute__((always_inline)) { return smem + (t & 1) * C::KTILE; };
   auto vbuf = [&](int t) __attribute__((always_inline)) {
     return smem + 2 * C::KTILE + (t & 1) * C::VTILE;
@@ -445,13 +466,13 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const uint16_t* vbase = a.v + (size_t)hk * D;
 
   auto compute = [&](int it) __attribute__((always_inline)) {
-    const int k0 = seg_lo + it * BK;
-    const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last);
+    const int k0 = k_lo + it * BK;
+    const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last + shift);
     if (!active) return;
     const uint32_t kra = lds_addr(kbuf(it)) + k_row * 2;
     const uint32_t ka = lds_addr(kbuf(it)) + k_tr * 2;
     const uint32_t vra = lds_addr(vbuf(it)) + v_row * 2;
-    const bool need_mask = (a.causal && k0 + BK - 1 > wrow0) || (k0 + BK > seg_hi);
+    const bool need_mask = (a.causal && k0 + BK - 1 > wrow0 + shift) || (k0 + BK > k_hi);
     // one 32-key block at a time keeps S^T and dP^T to 32 registers
     static_for<BK / 32>([&](auto KB) {
       constexpr int kb = decltype(KB)::value;
@@ -515,11 +536,12 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
     kd.init(kvstride);
     vd.init(kvstride);
     auto issue = [&](int t) __attribute__((always_inline)) {
-      const int kt = seg_lo + t * BK;
-      kd.issue(kbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, kbuf(t));
-      vd.issue(vbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, vbuf(t));
+      const int kt = k_lo + t * BK;
+      kd.issue(kbase + (size_t)kt * kvstride, kvstride, k_hi - kt, kbuf(t));
+      vd.issue(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt, vbuf(t));
     };
-    issue(0);
+    // (a chunk can leave a tile without any visible key tile, or with no keys)
+    if (ntiles > 0) issue(0);
     for (int it = 0; it < ntiles; ++it) {
       wait_dma();
       __syncthreads();
@@ -529,16 +551,18 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   } else {
     TileLoader<KL, BK, D, C::NT> kl;
     TileLoader<VL, BK, D, C::NT> vl;
-    kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-    vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-    kl.store(kbuf(0));
-    vl.store(vbuf(0));
+    if (ntiles > 0) {
+      kl.load_clamped(kbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
+      vl.load_clamped(vbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
+      kl.store(kbuf(0));
+      vl.store(vbuf(0));
+    }
     for (int it = 0; it < ntiles; ++it) {
       const bool more = it + 1 < ntiles;
       if (more) {
-        const int k1 = seg_lo + (it + 1) * BK;
-        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+        const int k1 = k_lo + (it + 1) * BK;
+        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
+        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
       }
       __syncthreads();
       compute(it);

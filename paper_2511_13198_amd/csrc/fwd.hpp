@@ -66,6 +66,13 @@ struct FwdArgs {
   int hkv;
   int causal;
   float scale_log2;  // scale * log2(e)
+  // chunk mode (chunked != 0): one query chunk of total_tokens rows over one
+  // key/value chunk of tk rows of the same sequence; key j is visible to
+  // row i (causal) iff j <= i + shift (shift = query offset - key offset).
+  // Otherwise rows and keys share the packed segments of cu.
+  int chunked;
+  int tk;
+  int shift;
 };
 
 // key offset within a 32-key block held in accumulator register r (lane half 0)
@@ -83,8 +90,13 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const int h = blockIdx.x % a.hq;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
-  const int seg_lo = a.cu[seg];
-  const int seg_hi = a.cu[seg + 1];
+  // query rows [seg_lo, seg_hi), keys [k_lo, k_hi); causal: key j visible to
+  // row i iff j <= i + shift
+  const int seg_lo = a.chunked ? 0 : a.cu[seg];
+  const int seg_hi = a.chunked ? a.total_tokens : a.cu[seg + 1];
+  const int k_lo = a.chunked ? 0 : seg_lo;
+  const int k_hi = a.chunked ? a.tk : seg_hi;
+  const int shift = a.chunked ? a.shift : 0;
   const int q0 = seg_lo + level * BQ;
   const int hk = h / (a.hq / a.hkv);
 
@@ -95,7 +107,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const int wrow0 = q0 + w * 32;
   const int wrow_last = wrow0 + 31;
   // last key this row may see
-  const int key_lim = a.causal ? min(row, seg_hi - 1) : seg_hi - 1;
+  const int key_lim = a.causal ? min(row + shift, k_hi - 1) : k_hi - 1;
 
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
@@ -116,8 +128,8 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   float lsum = 0.f;     // partial row sum over this lane's keys
   f32x16 s[BKS / 32];   // S^T of the keys in flight
 
-  const int kv_end = a.causal ? min(seg_hi, q0 + BQ) : seg_hi;
-  const int ntiles = (kv_end - seg_lo + BK - 1) / BK;
+  const int kv_end = a.causal ? min(k_hi, q0 + BQ + shift) : k_hi;
+  const int ntiles = max(0, (kv_end - k_lo + BK - 1) / BK);
 
   auto kbuf = [&](int t) __attribute__((always_inline)) {
     return smem + (t % C::STAGES) * (C::KTILE + C::VTILE);
@@ -126,7 +138,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const int k_lane = row_lane_base<KL>();
   const int v_lane = tr_lane_base<VL>();
   auto active = [&](int t) __attribute__((always_inline)) {
-    return (wrow0 < seg_hi) && (!a.causal || seg_lo + t * BK <= wrow_last);
+    return (wrow0 < seg_hi) && (!a.causal || k_lo + t * BK <= wrow_last + shift);
   };
 
   // S^T for the tile's 32-key blocks; the independent chains interleave
@@ -168,7 +180,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
 
   // mask, online softmax, then O^T += V^T P^T
   auto softmax_pv = [&](int k0, const uint16_t* vtile) __attribute__((always_inline)) {
-    const bool need_mask = (a.causal && k0 + BKS - 1 > wrow0) || (k0 + BKS > seg_hi);
+    const bool need_mask = (a.causal && k0 + BKS - 1 > wrow0 + shift) || (k0 + BKS > k_hi);
     if (need_mask) {
 #pragma unroll
       for (int kb = 0; kb < BKS / 32; ++kb) {
@@ -239,9 +251,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
     kd.init(kvstride);
     vd.init(kvstride);
     auto issue = [&](int t) __attribute__((always_inline)) {
-      const int kt = seg_lo + t * BK;
-      kd.issue(kbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, kbuf(t));
-      vd.issue(vbase + (size_t)kt * kvstride, kvstride, seg_hi - kt, vbuf(t));
+      const int kt = k_lo + t * BK;
+      kd.issue(kbase + (size_t)kt * kvstride, kvstride, k_hi - kt, kbuf(t));
+      vd.issue(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt, vbuf(t));
     };
     constexpr int S = C::STAGES;
     constexpr int PK = TileDma<KL, BK, NW>::PER_WAVE, PV = TileDma<VL, BK, NW>::PER_WAVE;
@@ -261,7 +273,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
       if (active(it)) {
         // the copies of tile tn go out one per K-step of S, so that they
         // trickle into the memory pipeline instead of queueing at once
-        const int kt = seg_lo + tn * BK;
+        const int kt = k_lo + tn * BK;
         const uint16_t* kg = kbase + (size_t)kt * kvstride;
         const uint16_t* vg = vbase + (size_t)kt * kvstride;
         uint16_t* kl = kbuf(tn);
@@ -269,17 +281,17 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
         auto copy = [&](auto CI) __attribute__((always_inline)) {
           constexpr int c = decltype(CI)::value;
           if constexpr (c < PK) {
-            if (more) kd.template issue_one<c>(kg, kvstride, seg_hi - kt, kl);
+            if (more) kd.template issue_one<c>(kg, kvstride, k_hi - kt, kl);
           } else if constexpr (c < PK + PV) {
-            if (more) vd.template issue_one<c - PK>(vg, kvstride, seg_hi - kt, vl);
+            if (more) vd.template issue_one<c - PK>(vg, kvstride, k_hi - kt, vl);
           }
         };
         // the tile is taken in softmax steps of BKS keys; the first step
         // issues the copies
         static_for<BK / BKS>([&](auto SUB) {
           constexpr int sub = decltype(SUB)::value;
-          const int k0s = seg_lo + it * BK + sub * BKS;
-          if (sub == 0 || (k0s < kv_end && (!a.causal || k0s <= wrow_last))) {
+          const int k0s = k_lo + it * BK + sub * BKS;
+          if (sub == 0 || (k0s < kv_end && (!a.causal || k0s <= wrow_last + shift))) {
             compute_s(kbuf(it) + sub * BKS * KL::ROW, [&](auto KS) __attribute__((always_inline)) {
               if constexpr (sub == 0) copy(KS);
             });
@@ -299,21 +311,23 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   } else {
     TileLoader<KL, BK, D, C::NT> kl;
     TileLoader<VL, BK, D, C::NT> vl;
-    kl.load_clamped(kbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-    vl.load_clamped(vbase + (size_t)seg_lo * kvstride, kvstride, seg_hi - seg_lo);
-    kl.store(kbuf(0));
-    vl.store(vbuf(0));
+    if (ntiles > 0) {
+      kl.load_clamped(kbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
+      vl.load_clamped(vbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
+      kl.store(kbuf(0));
+      vl.store(vbuf(0));
+    }
     for (int it = 0; it < ntiles; ++it) {
       const bool more = it + 1 < ntiles;
       if (more) {
-        const int k1 = seg_lo + (it + 1) * BK;
-        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
-        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, seg_hi - k1);
+        const int k1 = k_lo + (it + 1) * BK;
+        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
+        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
       }
       __syncthreads();
       if (active(it)) {
         compute_s(kbuf(it), no_hook);
-        softmax_pv(seg_lo + it * BK, vbuf(it));
+        softmax_pv(k_lo + it * BK, vbuf(it));
       }
       if (more) {
         kl.store(kbuf(it + 1));
@@ -325,7 +339,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   // epilogue: normalise, write O (bf16) and LSE (natural log)
   const float ltot = lsum + partner32(lsum);
   if (row < seg_hi) {
-    const float inv = 1.f / ltot;
+    // a row that saw no key (possible for a chunk) gets O = 0, LSE = -inf
+    const bool seen = ltot > 0.f;
+    const float inv = seen ? 1.f / ltot : 0.f;
     uint16_t* op = a.o + (size_t)row * qstride + (size_t)h * D;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -338,8 +354,58 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
         u32x2 pk = {__builtin_bit_cast(uint32_t, b01), __builtin_bit_cast(uint32_t, b23)};
         *reinterpret_cast<u32x2*>(op + db * 32 + g * 8 + hh * 4) = pk;
       }
-    if (hh == 0) a.lse[(size_t)h * a.total_tokens + row] = (m + __builtin_log2f(ltot)) * kLn2;
+    if (hh == 0)
+      a.lse[(size_t)h * a.total_tokens + row] = seen ? (m + __builtin_log2f(ltot)) * kLn2 : -INFINITY;
   }
+}
+
+// n floats set to zero, 4 per thread
+__global__ void __launch_bounds__(256) zero_kernel(float* __restrict__ p, size_t n) {
+  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (i + e < n) p[i + e] = 0.f;
+}
+
+// Combine two partial results of the same query rows (one per key chunk):
+//   LSE = log(exp(LSE_a) + exp(LSE_b)),  O = w_a O_a + w_b O_b,
+//   w_x = exp(LSE_x - LSE); a part with LSE = -inf has weight 0, and a row
+// where both are -inf stays O = 0, LSE = -inf.  One 8-element slice of a
+// row and head per thread; the output may alias either input.
+template <int D>
+__global__ void __launch_bounds__(256) merge_kernel(const uint16_t* oa, const float* la,
+                                                    const uint16_t* ob, const float* lb,
+                                                    uint16_t* o, float* lse, int total_tokens,
+                                                    int hq) {
+  constexpr int LANES = D / 8;
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t pair = gid / LANES;  // row * hq + head
+  const int sub = (int)(gid % LANES);
+  if (pair >= (size_t)total_tokens * hq) return;
+  const size_t row = pair / hq;
+  const int h = (int)(pair % hq);
+  const size_t li = (size_t)h * total_tokens + row;
+  const float xa = la[li], xb = lb[li];
+  const float mx = fmaxf(xa, xb);
+  float wa = 0.f, wb = 0.f, l = -INFINITY;
+  if (mx != -INFINITY) {
+    const float ea = __expf(xa - mx), eb = __expf(xb - mx);
+    const float tot = ea + eb;
+    wa = ea / tot;
+    wb = eb / tot;
+    l = mx + __logf(tot);
+  }
+  const u32x4 va = *reinterpret_cast<const u32x4*>(oa + pair * D + sub * 8);
+  const u32x4 vb = *reinterpret_cast<const u32x4*>(ob + pair * D + sub * 8);
+  u32x4 out;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f32x2 x = {wa * __uint_as_float(va[i] << 16) + wb * __uint_as_float(vb[i] << 16),
+               wa * __uint_as_float(va[i] & 0xffff0000u) + wb * __uint_as_float(vb[i] & 0xffff0000u)};
+    out[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
+  }
+  *reinterpret_cast<u32x4*>(o + pair * D + sub * 8) = out;
+  if (sub == 0) lse[li] = l;
 }
 
 }  // namespace pdy

@@ -210,12 +210,13 @@ pdy_status check_ptr(const void* p, const char* name) {
   return PDY_OK;
 }
 
+// cu == nullptr: one segment of s.T tokens
 pdy_status launch_plan(const int32_t* cu, int32_t* ws, const Sizes& s, int tile,
                        hipStream_t st) {
   const int nt = tiles_of(s, tile);
   hipError_t e = launch_timed(K_PLAN, st, [&] {
     hipLaunchKernelGGL(pdy::plan_kernel, dim3(1), dim3(pdy::kPlanThreads), 0, st, cu, (int)s.N,
-                       tile, nt, ws);
+                       tile, nt, (int)s.T, ws);
   });
   if (e != hipSuccess) return hip_fail(e, "plan_kernel launch");
   return PDY_OK;
@@ -252,6 +253,170 @@ size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
   return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s);
 }
 
+}  // extern "C"
+
+namespace {
+
+// One query chunk against one key/value chunk of the same sequence
+// (context-parallel step), or off: rows and keys share cu's segments.
+struct Chunk {
+  int on = 0;
+  int tk = 0;     // key/value rows
+  int shift = 0;  // query offset - key offset
+};
+
+pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu,
+                    const Sizes& s, int32_t causal, float scale, void* o, float* lse,
+                    void* workspace, size_t workspace_bytes, void* stream, const Chunk& c,
+                    const char* who) {
+  pdy_status st;
+  const int nw = fwd_waves(s);
+  const int tile = 32 * nw;
+  const size_t need = plan_bytes(s, tile);
+  if (workspace_bytes < need)
+    return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
+                need);
+  hipError_t e = init_kernels();
+  if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  int32_t* ws = reinterpret_cast<int32_t*>(workspace);
+  if ((st = launch_plan(cu, ws, s, tile, hs)) != PDY_OK) return st;
+
+  pdy::FwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.cu = cu;
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.plan = make_plan(ws, s, tile);
+  a.total_tokens = (int)s.T;
+  a.hq = (int)s.hq;
+  a.hkv = (int)s.hkv;
+  a.causal = causal;
+  a.scale_log2 = scale * pdy::kLog2e;
+  a.chunked = c.on;
+  a.tk = c.tk;
+  a.shift = c.shift;
+  const dim3 grid((unsigned)(grid_items(s, tile) * s.hq));
+  e = launch_timed(K_FWD, hs, [&] {
+    if (s.d == 64) {
+      if (nw == 8) launch_fwd<64, 8>(grid, hs, a);
+      else launch_fwd<64, 4>(grid, hs, a);
+    } else {
+      if (nw == 8) launch_fwd<128, 8>(grid, hs, a);
+      else launch_fwd<128, 4>(grid, hs, a);
+    }
+  });
+  if (e != hipSuccess) return hip_fail(e, "fwd_kernel launch");
+  return PDY_OK;
+}
+
+// sk: sizes of the key side (the query side for self-attention)
+size_t bwd_need(const Sizes& s, const Sizes& sk) {
+  return plan_bytes(sk, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s);
+}
+
+pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                    const void* dout, const int32_t* cu, const Sizes& s, const Sizes& sk,
+                    int32_t causal, float scale, float* dq, float* dk, float* dv,
+                    void* workspace, size_t workspace_bytes, void* stream, const Chunk& c,
+                    const char* who) {
+  pdy_status st;
+  const int nwq = fwd_waves(s);
+  const int qtile = 32 * nwq;
+  const size_t need = bwd_need(s, sk);
+  if (workspace_bytes < need)
+    return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
+                need);
+  hipError_t e = init_kernels();
+  if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  int32_t* ws = reinterpret_cast<int32_t*>(workspace);
+  int32_t* ws_q = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) +
+                                              plan_bytes(sk, kTile));
+  float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) +
+                                       plan_bytes(sk, kTile) + plan_bytes(s, qtile));
+
+  if (sk.T > 0 && (st = launch_plan(cu, ws, sk, kTile, hs)) != PDY_OK) return st;
+  if ((st = launch_plan(cu, ws_q, s, qtile, hs)) != PDY_OK) return st;
+  {
+    const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    e = launch_timed(K_PRE, hs, [&] {
+      if (s.d == 64)
+        hipLaunchKernelGGL(pdy::bwd_pre_kernel<64>, dim3(blocks), dim3(256), 0, hs,
+                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
+                           (int)s.T, (int)s.hq);
+      else
+        hipLaunchKernelGGL(pdy::bwd_pre_kernel<128>, dim3(blocks), dim3(256), 0, hs,
+                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
+                           (int)s.T, (int)s.hq);
+    });
+    if (e != hipSuccess) return hip_fail(e, "bwd_pre_kernel launch");
+  }
+  pdy::BwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.lse = lse;
+  a.dd = dd;
+  a.cu = cu;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.plan = make_plan(ws, sk, kTile);
+  a.plan_q = make_plan(ws_q, s, qtile);
+  a.total_tokens = (int)s.T;
+  a.hq = (int)s.hq;
+  a.hkv = (int)s.hkv;
+  a.causal = causal;
+  a.scale = scale;
+  a.scale_log2 = scale * pdy::kLog2e;
+  a.chunked = c.on;
+  a.tk = c.tk;
+  a.shift = c.shift;
+  if (sk.T > 0) {
+    const dim3 gkv((unsigned)(grid_items(sk, kTile) * s.hkv));
+    e = launch_timed(K_DKDV, hs, [&] {
+      if (s.d == 64)
+        hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
+                           pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
+      else
+        hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
+                           pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
+    });
+    if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
+  }
+  const dim3 gq((unsigned)(grid_items(s, qtile) * s.hq));
+  e = launch_timed(K_DQ, hs, [&] {
+    if (s.d == 64) {
+      if (nwq == 8) launch_dq<64, 8>(gq, hs, a);
+      else launch_dq<64, 4>(gq, hs, a);
+    } else {
+      if (nwq == 8) launch_dq<128, 8>(gq, hs, a);
+      else launch_dq<128, 4>(gq, hs, a);
+    }
+  });
+  if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
+  return PDY_OK;
+}
+
+// sizes of a chunk: one segment of t tokens
+pdy_status chunk_sizes(int32_t tq, int32_t tk, int32_t hq, int32_t hkv, int32_t d, Sizes* sq,
+                       Sizes* sk) {
+  pdy_status st;
+  if (tq < 0 || tk < 0) return fail(PDY_ERR_INVALID_ARG, "chunk lengths must be >= 0");
+  if ((st = check_sizes(tq, 1, tq, hq, hkv, d, sq)) != PDY_OK) return st;
+  if ((st = check_sizes(tk, 1, tk, hq, hkv, d, sk)) != PDY_OK) return st;
+  return PDY_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
                     int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen, int32_t num_heads_q,
                     int32_t num_heads_kv, int32_t head_dim, int32_t causal, float scale, void* o,
@@ -271,43 +436,45 @@ pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* 
   if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
   if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
     return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
-  const int nw = fwd_waves(s);
-  const int tile = 32 * nw;
-  const size_t need = plan_bytes(s, tile);
-  if (workspace_bytes < need)
-    return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, attn_fwd needs %zu", workspace_bytes,
-                need);
-  hipError_t e = init_kernels();
-  if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
-  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  int32_t* ws = reinterpret_cast<int32_t*>(workspace);
-  if ((st = launch_plan(cu_seqlens, ws, s, tile, hs)) != PDY_OK) return st;
+  return fwd_impl(q, k, v, cu_seqlens, s, causal, scale, o, lse, workspace, workspace_bytes,
+                  stream, Chunk{}, "attn_fwd");
+}
 
-  pdy::FwdArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k = static_cast<const uint16_t*>(k);
-  a.v = static_cast<const uint16_t*>(v);
-  a.cu = cu_seqlens;
-  a.o = static_cast<uint16_t*>(o);
-  a.lse = lse;
-  a.plan = make_plan(ws, s, tile);
-  a.total_tokens = (int)s.T;
-  a.hq = (int)s.hq;
-  a.hkv = (int)s.hkv;
-  a.causal = causal;
-  a.scale_log2 = scale * pdy::kLog2e;
-  const dim3 grid((unsigned)(grid_items(s, tile) * s.hq));
-  e = launch_timed(K_FWD, hs, [&] {
-    if (s.d == 64) {
-      if (nw == 8) launch_fwd<64, 8>(grid, hs, a);
-      else launch_fwd<64, 4>(grid, hs, a);
-    } else {
-      if (nw == 8) launch_fwd<128, 8>(grid, hs, a);
-      else launch_fwd<128, 4>(grid, hs, a);
-    }
-  });
-  if (e != hipSuccess) return hip_fail(e, "fwd_kernel launch");
-  return PDY_OK;
+size_t attn_fwd_chunk_workspace_size(int32_t tq, int32_t tk, int32_t hq, int32_t hkv, int32_t d) {
+  Sizes sq, sk;
+  if (chunk_sizes(tq, tk, hq, hkv, d, &sq, &sk) != PDY_OK) return 0;
+  return plan_bytes(sq, 32 * fwd_waves(sq));
+}
+
+size_t attn_bwd_chunk_workspace_size(int32_t tq, int32_t tk, int32_t hq, int32_t hkv, int32_t d) {
+  Sizes sq, sk;
+  if (chunk_sizes(tq, tk, hq, hkv, d, &sq, &sk) != PDY_OK) return 0;
+  return bwd_need(sq, sk);
+}
+
+pdy_status attn_fwd_chunk(const void* q, const void* k, const void* v, int32_t tq, int32_t tk,
+                          int32_t q_offset, int32_t k_offset, int32_t num_heads_q,
+                          int32_t num_heads_kv, int32_t head_dim, int32_t causal, float scale,
+                          void* o, float* lse, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  g_err[0] = 0;
+  Sizes sq, sk;
+  pdy_status st;
+  if ((st = chunk_sizes(tq, tk, num_heads_q, num_heads_kv, head_dim, &sq, &sk)) != PDY_OK)
+    return st;
+  if (q_offset < 0 || k_offset < 0) return fail(PDY_ERR_INVALID_ARG, "offsets must be >= 0");
+  if ((st = check_scale(scale, causal)) != PDY_OK) return st;
+  if (tq == 0) return PDY_OK;
+  if ((st = check_ptr(q, "q")) || (st = check_ptr(o, "o")) || (st = check_ptr(lse, "lse")) ||
+      (st = check_ptr(workspace, "workspace")))
+    return st;
+  if (tk > 0 && ((st = check_ptr(k, "k")) || (st = check_ptr(v, "v")))) return st;
+  Chunk c;
+  c.on = 1;
+  c.tk = tk;
+  c.shift = q_offset - k_offset;
+  return fwd_impl(q, k, v, nullptr, sq, causal, scale, o, lse, workspace, workspace_bytes, stream,
+                  c, "attn_fwd_chunk");
 }
 
 pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
@@ -332,78 +499,80 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
   if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
     return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
-  const int nwq = fwd_waves(s);
-  const int qtile = 32 * nwq;
-  const size_t need = plan_bytes(s, kTile) + plan_bytes(s, qtile) + dd_bytes(s);
-  if (workspace_bytes < need)
-    return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, attn_bwd needs %zu", workspace_bytes,
-                need);
-  hipError_t e = init_kernels();
-  if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
-  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  int32_t* ws = reinterpret_cast<int32_t*>(workspace);
-  int32_t* ws_q = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) +
-                                              plan_bytes(s, kTile));
-  float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) +
-                                       plan_bytes(s, kTile) + plan_bytes(s, qtile));
+  return bwd_impl(q, k, v, o, lse, dout, cu_seqlens, s, s, causal, scale, dq, dk, dv, workspace,
+                  workspace_bytes, stream, Chunk{}, "attn_bwd");
+}
 
-  if ((st = launch_plan(cu_seqlens, ws, s, kTile, hs)) != PDY_OK) return st;
-  if ((st = launch_plan(cu_seqlens, ws_q, s, qtile, hs)) != PDY_OK) return st;
-  {
-    const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
-    const unsigned blocks = (unsigned)((threads + 255) / 256);
-    e = launch_timed(K_PRE, hs, [&] {
-      if (s.d == 64)
-        hipLaunchKernelGGL(pdy::bwd_pre_kernel<64>, dim3(blocks), dim3(256), 0, hs,
-                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
-                           (int)s.T, (int)s.hq);
-      else
-        hipLaunchKernelGGL(pdy::bwd_pre_kernel<128>, dim3(blocks), dim3(256), 0, hs,
-                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
-                           (int)s.T, (int)s.hq);
-    });
-    if (e != hipSuccess) return hip_fail(e, "bwd_pre_kernel launch");
+pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const void* o,
+                          const float* lse, const void* dout, int32_t tq, int32_t tk,
+                          int32_t q_offset, int32_t k_offset, int32_t num_heads_q,
+                          int32_t num_heads_kv, int32_t head_dim, int32_t causal, float scale,
+                          float* dq, float* dk, float* dv, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  Sizes sq, sk;
+  pdy_status st;
+  if ((st = chunk_sizes(tq, tk, num_heads_q, num_heads_kv, head_dim, &sq, &sk)) != PDY_OK)
+    return st;
+  if (q_offset < 0 || k_offset < 0) return fail(PDY_ERR_INVALID_ARG, "offsets must be >= 0");
+  if ((st = check_scale(scale, causal)) != PDY_OK) return st;
+  if (tq == 0 && tk == 0) return PDY_OK;
+  if (tq > 0 && ((st = check_ptr(q, "q")) || (st = check_ptr(o, "o")) ||
+                 (st = check_ptr(lse, "lse")) || (st = check_ptr(dout, "dout")) ||
+                 (st = check_ptr(dq, "dq"))))
+    return st;
+  if (tk > 0 && ((st = check_ptr(k, "k")) || (st = check_ptr(v, "v")) ||
+                 (st = check_ptr(dk, "dk")) || (st = check_ptr(dv, "dv"))))
+    return st;
+  if ((st = check_ptr(workspace, "workspace")) != PDY_OK) return st;
+  if (tq == 0) {
+    // no query rows: the key chunk receives no gradient (a fill kernel, not
+    // a memset, so that the call can be captured in a graph)
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    const size_t n = (size_t)tk * num_heads_kv * head_dim;
+    const unsigned blocks = (unsigned)((n + 1023) / 1024);
+    hipLaunchKernelGGL(pdy::zero_kernel, dim3(blocks), dim3(256), 0, hs, dk, n);
+    hipLaunchKernelGGL(pdy::zero_kernel, dim3(blocks), dim3(256), 0, hs, dv, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "zero_kernel launch");
+    return PDY_OK;
   }
-  pdy::BwdArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k = static_cast<const uint16_t*>(k);
-  a.v = static_cast<const uint16_t*>(v);
-  a.dout = static_cast<const uint16_t*>(dout);
-  a.lse = lse;
-  a.dd = dd;
-  a.cu = cu_seqlens;
-  a.dq = dq;
-  a.dk = dk;
-  a.dv = dv;
-  a.plan = make_plan(ws, s, kTile);
-  a.plan_q = make_plan(ws_q, s, qtile);
-  a.total_tokens = (int)s.T;
-  a.hq = (int)s.hq;
-  a.hkv = (int)s.hkv;
-  a.causal = causal;
-  a.scale = scale;
-  a.scale_log2 = scale * pdy::kLog2e;
-  const dim3 gkv((unsigned)(grid_items(s, kTile) * s.hkv));
-  const dim3 gq((unsigned)(grid_items(s, qtile) * s.hq));
-  e = launch_timed(K_DKDV, hs, [&] {
-    if (s.d == 64)
-      hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
-                         pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
-    else
-      hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
-                         pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
-  });
-  if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
-  e = launch_timed(K_DQ, hs, [&] {
-    if (s.d == 64) {
-      if (nwq == 8) launch_dq<64, 8>(gq, hs, a);
-      else launch_dq<64, 4>(gq, hs, a);
-    } else {
-      if (nwq == 8) launch_dq<128, 8>(gq, hs, a);
-      else launch_dq<128, 4>(gq, hs, a);
-    }
-  });
-  if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
+  Chunk c;
+  c.on = 1;
+  c.tk = tk;
+  c.shift = q_offset - k_offset;
+  return bwd_impl(q, k, v, o, lse, dout, nullptr, sq, sk, causal, scale, dq, dk, dv, workspace,
+                  workspace_bytes, stream, c, "attn_bwd_chunk");
+}
+
+pdy_status attn_merge(const void* o_a, const float* lse_a, const void* o_b, const float* lse_b,
+                      int32_t total_tokens, int32_t num_heads_q, int32_t head_dim, void* o,
+                      float* lse, void* stream) {
+  g_err[0] = 0;
+  pdy_status st;
+  if (total_tokens < 0) return fail(PDY_ERR_INVALID_ARG, "total_tokens must be >= 0");
+  if (num_heads_q < 1) return fail(PDY_ERR_INVALID_ARG, "num_heads_q must be >= 1");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PDY_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", head_dim);
+  if (total_tokens == 0) return PDY_OK;
+  if ((st = check_ptr(o_a, "o_a")) || (st = check_ptr(lse_a, "lse_a")) ||
+      (st = check_ptr(o_b, "o_b")) || (st = check_ptr(lse_b, "lse_b")) ||
+      (st = check_ptr(o, "o")) || (st = check_ptr(lse, "lse")))
+    return st;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const size_t threads = (size_t)total_tokens * num_heads_q * (head_dim / 8);
+  const unsigned blocks = (unsigned)((threads + 255) / 256);
+  const auto* a = static_cast<const uint16_t*>(o_a);
+  const auto* b = static_cast<const uint16_t*>(o_b);
+  auto* out = static_cast<uint16_t*>(o);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(pdy::merge_kernel<64>, dim3(blocks), dim3(256), 0, hs, a, lse_a, b, lse_b,
+                       out, lse, (int)total_tokens, (int)num_heads_q);
+  else
+    hipLaunchKernelGGL(pdy::merge_kernel<128>, dim3(blocks), dim3(256), 0, hs, a, lse_a, b, lse_b,
+                       out, lse, (int)total_tokens, (int)num_heads_q);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "merge_kernel launch");
   return PDY_OK;
 }
 

@@ -21,8 +21,10 @@ __host__ __device__ inline size_t plan_ints(int n, int max_nt) {
   return (size_t)2 * n + (size_t)2 * max_nt + 1;
 }
 
+// cu == nullptr: a single segment of single_len tokens (n must be 1)
 __global__ void __launch_bounds__(kPlanThreads)
-plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int32_t* __restrict__ ws) {
+plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int single_len,
+            int32_t* __restrict__ ws) {
   int32_t* nt = ws;
   int32_t* order = nt + n;
   int32_t* cnt = order + n;
@@ -33,7 +35,7 @@ plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int32_t* 
 
   // 1. tiles per segment
   for (int s = t; s < n; s += kPlanThreads) {
-    const int len = cu[s + 1] - cu[s];
+    const int len = cu ? cu[s + 1] - cu[s] : single_len;
     int v = (len + bt - 1) / bt;
     nt[s] = v < max_nt ? v : max_nt;  // max_seqlen is a caller-guaranteed bound
   }

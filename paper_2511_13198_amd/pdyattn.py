@@ -23,6 +23,8 @@ PDY_ERR_HIP = -4
 
 # exported symbols, in the order include/pdyattn.h declares them
 SYMBOLS = ("attn_fwd_workspace_size", "attn_bwd_workspace_size", "attn_fwd", "attn_bwd",
+           "attn_fwd_chunk_workspace_size", "attn_bwd_chunk_workspace_size", "attn_fwd_chunk",
+           "attn_bwd_chunk", "attn_merge",
            "attn_validate_cu_seqlens", "pdy_status_string", "pdy_last_error",
            "pdy_kernel_count", "pdy_kernel_name", "pdy_profile_start", "pdy_profile_stop")
 
@@ -55,6 +57,18 @@ def lib() -> ctypes.CDLL:
     L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
                            vp, vp, vp, vp, sz, vp]
     L.attn_bwd.restype = i32
+    L.attn_fwd_chunk_workspace_size.argtypes = [i32] * 5
+    L.attn_fwd_chunk_workspace_size.restype = sz
+    L.attn_bwd_chunk_workspace_size.argtypes = [i32] * 5
+    L.attn_bwd_chunk_workspace_size.restype = sz
+    L.attn_fwd_chunk.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, f32, vp, vp,
+                                 vp, sz, vp]
+    L.attn_fwd_chunk.restype = i32
+    L.attn_bwd_chunk.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32,
+                                 f32, vp, vp, vp, vp, sz, vp]
+    L.attn_bwd_chunk.restype = i32
+    L.attn_merge.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp]
+    L.attn_merge.restype = i32
     L.attn_validate_cu_seqlens.argtypes = [vp, i32, i32, ctypes.POINTER(i32), vp]
     L.attn_validate_cu_seqlens.restype = i32
     L.pdy_status_string.argtypes = [i32]
@@ -211,3 +225,98 @@ def attn_bwd(q, k, v, o, lse, dout, cu_seqlens, max_seqlen: Optional[int] = None
                         workspace.numel() * workspace.element_size(), _stream_handle(q.device))
     _check(st, "attn_bwd")
     return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# One long sequence split into chunks (context parallelism)
+# ---------------------------------------------------------------------------
+def fwd_chunk_workspace_size(tq, tk, hq, hkv, d) -> int:
+    return int(lib().attn_fwd_chunk_workspace_size(tq, tk, hq, hkv, d))
+
+
+def bwd_chunk_workspace_size(tq, tk, hq, hkv, d) -> int:
+    return int(lib().attn_bwd_chunk_workspace_size(tq, tk, hq, hkv, d))
+
+
+def _ptr(t):
+    return 0 if t is None else t.data_ptr()
+
+
+def attn_fwd_chunk(q, k, v, q_offset: int, k_offset: int, causal: bool = True,
+                   scale: Optional[float] = None, out=None, lse=None, workspace=None):
+    """Partial O [Tq, Hq, d] bf16 and LSE [Hq, Tq] fp32 of the query chunk at
+    positions q_offset.. over the key/value chunk at positions k_offset.."""
+    import torch
+    _check_tensor(q, "q", torch.bfloat16, 3)
+    _check_tensor(k, "k", torch.bfloat16, 3)
+    _check_tensor(v, "v", torch.bfloat16, 3)
+    tq, hq, d = q.shape
+    tk, hkv = k.shape[0], k.shape[1]
+    if tuple(v.shape) != tuple(k.shape) or k.shape[2] != d:
+        raise ValueError("k and v must be [Tk, Hkv, d] with q's d")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((hq, tq), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = _ws(fwd_chunk_workspace_size(tq, tk, hq, hkv, d), q.device)
+    st = lib().attn_fwd_chunk(q.data_ptr(), _ptr(k) if tk else 0, _ptr(v) if tk else 0, tq, tk,
+                              int(q_offset), int(k_offset), hq, hkv, d, int(bool(causal)),
+                              float(scale), out.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
+                              workspace.numel() * workspace.element_size(),
+                              _stream_handle(q.device))
+    _check(st, "attn_fwd_chunk")
+    return out, lse
+
+
+def attn_bwd_chunk(q, k, v, o, lse, dout, q_offset: int, k_offset: int, causal: bool = True,
+                   scale: Optional[float] = None, dq=None, dk=None, dv=None, workspace=None):
+    """This (query chunk, key chunk) pair's part of dQ [Tq, Hq, d] and dK, dV
+    [Tk, Hkv, d] (fp32), given the final o and lse of the query rows."""
+    import torch
+    for t, name in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
+        _check_tensor(t, name, torch.bfloat16, 3)
+    _check_tensor(lse, "lse", torch.float32, 2)
+    tq, hq, d = q.shape
+    tk, hkv = k.shape[0], k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    dev = q.device if tq else k.device
+    if dq is None:
+        dq = torch.empty((tq, hq, d), dtype=torch.float32, device=dev)
+    if dk is None:
+        dk = torch.empty((tk, hkv, d), dtype=torch.float32, device=dev)
+    if dv is None:
+        dv = torch.empty((tk, hkv, d), dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = _ws(bwd_chunk_workspace_size(tq, tk, hq, hkv, d), dev)
+    st = lib().attn_bwd_chunk(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                              lse.data_ptr(), dout.data_ptr(), tq, tk, int(q_offset),
+                              int(k_offset), hq, hkv, d, int(bool(causal)), float(scale),
+                              dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), workspace.data_ptr(),
+                              workspace.numel() * workspace.element_size(), _stream_handle(dev))
+    _check(st, "attn_bwd_chunk")
+    return dq, dk, dv
+
+
+def attn_merge(o_a, lse_a, o_b, lse_b, out=None, lse=None):
+    """Combine two partial (O, LSE) of the same rows; out/lse may be o_a/lse_a."""
+    import torch
+    _check_tensor(o_a, "o_a", torch.bfloat16, 3)
+    _check_tensor(o_b, "o_b", torch.bfloat16, 3)
+    _check_tensor(lse_a, "lse_a", torch.float32, 2)
+    _check_tensor(lse_b, "lse_b", torch.float32, 2)
+    T, hq, d = o_a.shape
+    if tuple(o_b.shape) != (T, hq, d) or tuple(lse_a.shape) != (hq, T) or \
+            tuple(lse_b.shape) != (hq, T):
+        raise ValueError("partials must share shapes [T, Hq, d] and [Hq, T]")
+    if out is None:
+        out = torch.empty_like(o_a)
+    if lse is None:
+        lse = torch.empty_like(lse_a)
+    st = lib().attn_merge(o_a.data_ptr(), lse_a.data_ptr(), o_b.data_ptr(), lse_b.data_ptr(), T,
+                          hq, d, out.data_ptr(), lse.data_ptr(), _stream_handle(o_a.device))
+    _check(st, "attn_merge")
+    return out, lse

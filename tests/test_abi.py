@@ -110,3 +110,67 @@ def test_status_strings_and_kernel_names():
     # profiling with nothing launched reports nothing
     P.profile_start()
     assert P.profile_stop() == {}
+
+
+def _fwd_chunk(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, tq=256, tk=256, qo=0, ko=0, hq=4, hkv=2, d=128, causal=1,
+             scale=0.1, o=FAKE, lse=FAKE, ws=FAKE, wsb=1 << 20, stream=None)
+    a.update(kw)
+    return P.lib().attn_fwd_chunk(a["q"], a["k"], a["v"], a["tq"], a["tk"], a["qo"], a["ko"],
+                                  a["hq"], a["hkv"], a["d"], a["causal"], a["scale"], a["o"],
+                                  a["lse"], a["ws"], a["wsb"], a["stream"])
+
+
+def _bwd_chunk(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, do=FAKE, tq=256, tk=256, qo=0, ko=0, hq=4,
+             hkv=2, d=128, causal=1, scale=0.1, dq=FAKE, dk=FAKE, dv=FAKE, ws=FAKE, wsb=1 << 30,
+             stream=None)
+    a.update(kw)
+    return P.lib().attn_bwd_chunk(a["q"], a["k"], a["v"], a["o"], a["lse"], a["do"], a["tq"],
+                                  a["tk"], a["qo"], a["ko"], a["hq"], a["hkv"], a["d"],
+                                  a["causal"], a["scale"], a["dq"], a["dk"], a["dv"], a["ws"],
+                                  a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(tq=-1), P.PDY_ERR_INVALID_ARG, "chunk lengths"),
+    (dict(ko=-5), P.PDY_ERR_INVALID_ARG, "offsets"),
+    (dict(d=96), P.PDY_ERR_UNSUPPORTED, "head_dim"),
+    (dict(hq=6, hkv=4), P.PDY_ERR_INVALID_ARG, "multiple"),
+    (dict(scale=-1.0), P.PDY_ERR_INVALID_ARG, "scale"),
+    (dict(o=0), P.PDY_ERR_INVALID_ARG, "o is NULL"),
+    (dict(k=0), P.PDY_ERR_INVALID_ARG, "k is NULL"),
+    (dict(wsb=8), P.PDY_ERR_WORKSPACE, "attn_fwd_chunk"),
+])
+def test_fwd_chunk_argument_errors(kw, status, msg):
+    st = _fwd_chunk(**kw)
+    assert st == status, (st, P.last_error())
+    assert msg in P.last_error()
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(tk=-1), P.PDY_ERR_INVALID_ARG, "chunk lengths"),
+    (dict(qo=-1), P.PDY_ERR_INVALID_ARG, "offsets"),
+    (dict(dv=0), P.PDY_ERR_INVALID_ARG, "dv is NULL"),
+    (dict(lse=FAKE + 4), P.PDY_ERR_INVALID_ARG, "aligned"),
+    (dict(wsb=64), P.PDY_ERR_WORKSPACE, "attn_bwd_chunk"),
+])
+def test_bwd_chunk_argument_errors(kw, status, msg):
+    st = _bwd_chunk(**kw)
+    assert st == status, (st, P.last_error())
+    assert msg in P.last_error()
+
+
+def test_chunk_noops_and_workspace_sizes():
+    # no query rows: nothing to do (k and v may be absent)
+    assert _fwd_chunk(tq=0, q=0, k=0, v=0, o=0, lse=0, ws=0, wsb=0) == P.PDY_OK
+    assert _bwd_chunk(tq=0, tk=0, q=0, k=0, v=0, o=0, lse=0, do=0, dq=0, dk=0, dv=0, ws=0,
+                      wsb=0) == P.PDY_OK
+    f = P.fwd_chunk_workspace_size(4096, 8192, 4, 4, 128)
+    b = P.bwd_chunk_workspace_size(4096, 8192, 4, 4, 128)
+    assert 256 <= f < 1 << 20 and b >= 4 * 4096 * 4
+    assert P.fwd_chunk_workspace_size(-1, 5, 4, 4, 128) == 0
+    L = P.lib()
+    assert L.attn_merge(FAKE, FAKE, FAKE, FAKE, 10, 4, 96, FAKE, FAKE, None) == P.PDY_ERR_UNSUPPORTED
+    assert L.attn_merge(FAKE, FAKE, FAKE, FAKE, 0, 4, 128, 0, 0, None) == P.PDY_OK
+    assert L.attn_merge(FAKE, 0, FAKE, FAKE, 10, 4, 128, FAKE, FAKE, None) == P.PDY_ERR_INVALID_ARG
