@@ -123,14 +123,16 @@ pdy_status attn_fwd_chunk(const void* q, const void* k, const void* v, int32_t t
  * rows (merged over every key chunk), dout their upstream gradient.
  * Writes dq fp32 [tq, Hq, d] (this pair's part; the chunk's dQ is the sum
  * over its key chunks) and dk, dv fp32 [tk, Hkv, d] (this pair's part; a key
- * chunk's gradient is the sum over query chunks).  Rows with lse = -inf
- * contribute nothing.  tq = 0 writes zero dk, dv. */
+ * chunk's gradient is the sum over query chunks); with accumulate = 1 the
+ * part is added to what dq, dk and dv hold.  Rows with lse = -inf
+ * contribute nothing.  tq = 0 writes zero dk, dv (accumulate = 0) or leaves
+ * them (accumulate = 1). */
 pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const void* o,
                           const float* lse, const void* dout, int32_t tq, int32_t tk,
                           int32_t q_offset, int32_t k_offset,
                           int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
                           int32_t causal, float scale,
-                          float* dq, float* dk, float* dv,
+                          float* dq, float* dk, float* dv, int32_t accumulate,
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* Combine two partial results of the same T query rows:

@@ -83,6 +83,7 @@ struct BwdArgs {
   int chunked;
   int tk;
   int shift;
+  int accumulate;  // add to dq/dk/dv instead of overwriting them
 };
 
 // dK/dV: one workgroup of 8 waves per (segment, kv head, 128-key tile).  Waves
@@ -381,6 +382,10 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
           kv[e] = (dka[db][r] + red[(db * 16 + r) * 64 + l]) * a.scale;
           vv[e] = dva[db][r] + red[32 * D + (db * 16 + r) * 64 + l];
         }
+        if (a.accumulate) {
+          kv += *reinterpret_cast<const f32x4*>(dkp + d0);
+          vv += *reinterpret_cast<const f32x4*>(dvp + d0);
+        }
         *reinterpret_cast<f32x4*>(dkp + d0) = kv;
         *reinterpret_cast<f32x4*>(dvp + d0) = vv;
       }
@@ -582,6 +587,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
         const int d0 = db * 32 + grp * 8 + hh * 4;
         f32x4 v = {dqa[db][grp * 4] * a.scale, dqa[db][grp * 4 + 1] * a.scale,
                    dqa[db][grp * 4 + 2] * a.scale, dqa[db][grp * 4 + 3] * a.scale};
+        if (a.accumulate) v += *reinterpret_cast<const f32x4*>(dqp + d0);
         *reinterpret_cast<f32x4*>(dqp + d0) = v;
       }
   }

@@ -261,8 +261,9 @@ namespace {
 // (context-parallel step), or off: rows and keys share cu's segments.
 struct Chunk {
   int on = 0;
-  int tk = 0;     // key/value rows
-  int shift = 0;  // query offset - key offset
+  int tk = 0;          // key/value rows
+  int shift = 0;       // query offset - key offset
+  int accumulate = 0;  // backward: add to the gradients instead of writing them
 };
 
 pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu,
@@ -377,6 +378,7 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   a.chunked = c.on;
   a.tk = c.tk;
   a.shift = c.shift;
+  a.accumulate = c.accumulate;
   if (sk.T > 0) {
     const dim3 gkv((unsigned)(grid_items(sk, kTile) * s.hkv));
     e = launch_timed(K_DKDV, hs, [&] {
@@ -507,7 +509,7 @@ pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const voi
                           const float* lse, const void* dout, int32_t tq, int32_t tk,
                           int32_t q_offset, int32_t k_offset, int32_t num_heads_q,
                           int32_t num_heads_kv, int32_t head_dim, int32_t causal, float scale,
-                          float* dq, float* dk, float* dv, void* workspace,
+                          float* dq, float* dk, float* dv, int32_t accumulate, void* workspace,
                           size_t workspace_bytes, void* stream) {
   g_err[0] = 0;
   Sizes sq, sk;
@@ -524,7 +526,10 @@ pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const voi
   if (tk > 0 && ((st = check_ptr(k, "k")) || (st = check_ptr(v, "v")) ||
                  (st = check_ptr(dk, "dk")) || (st = check_ptr(dv, "dv"))))
     return st;
+  if (accumulate != 0 && accumulate != 1)
+    return fail(PDY_ERR_INVALID_ARG, "accumulate must be 0 or 1 (got %d)", accumulate);
   if ((st = check_ptr(workspace, "workspace")) != PDY_OK) return st;
+  if (tq == 0 && accumulate) return PDY_OK;
   if (tq == 0) {
     // no query rows: the key chunk receives no gradient (a fill kernel, not
     // a memset, so that the call can be captured in a graph)
@@ -541,6 +546,7 @@ pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const voi
   c.on = 1;
   c.tk = tk;
   c.shift = q_offset - k_offset;
+  c.accumulate = accumulate;
   return bwd_impl(q, k, v, o, lse, dout, nullptr, sq, sk, causal, scale, dq, dk, dv, workspace,
                   workspace_bytes, stream, c, "attn_bwd_chunk");
 }

@@ -65,7 +65,7 @@ def lib() -> ctypes.CDLL:
                                  vp, sz, vp]
     L.attn_fwd_chunk.restype = i32
     L.attn_bwd_chunk.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32,
-                                 f32, vp, vp, vp, vp, sz, vp]
+                                 f32, vp, vp, vp, i32, vp, sz, vp]
     L.attn_bwd_chunk.restype = i32
     L.attn_merge.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, vp]
     L.attn_merge.restype = i32
@@ -272,9 +272,11 @@ def attn_fwd_chunk(q, k, v, q_offset: int, k_offset: int, causal: bool = True,
 
 
 def attn_bwd_chunk(q, k, v, o, lse, dout, q_offset: int, k_offset: int, causal: bool = True,
-                   scale: Optional[float] = None, dq=None, dk=None, dv=None, workspace=None):
+                   scale: Optional[float] = None, dq=None, dk=None, dv=None, workspace=None,
+                   accumulate: bool = False):
     """This (query chunk, key chunk) pair's part of dQ [Tq, Hq, d] and dK, dV
-    [Tk, Hkv, d] (fp32), given the final o and lse of the query rows."""
+    [Tk, Hkv, d] (fp32), given the final o and lse of the query rows; with
+    accumulate=True it is added to the given dq, dk, dv."""
     import torch
     for t, name in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
         _check_tensor(t, name, torch.bfloat16, 3)
@@ -295,8 +297,9 @@ def attn_bwd_chunk(q, k, v, o, lse, dout, q_offset: int, k_offset: int, causal: 
     st = lib().attn_bwd_chunk(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                               lse.data_ptr(), dout.data_ptr(), tq, tk, int(q_offset),
                               int(k_offset), hq, hkv, d, int(bool(causal)), float(scale),
-                              dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), workspace.data_ptr(),
-                              workspace.numel() * workspace.element_size(), _stream_handle(dev))
+                              dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), int(bool(accumulate)),
+                              workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                              _stream_handle(dev))
     _check(st, "attn_bwd_chunk")
     return dq, dk, dv
 

@@ -123,13 +123,13 @@ def _fwd_chunk(**kw):
 
 def _bwd_chunk(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, do=FAKE, tq=256, tk=256, qo=0, ko=0, hq=4,
-             hkv=2, d=128, causal=1, scale=0.1, dq=FAKE, dk=FAKE, dv=FAKE, ws=FAKE, wsb=1 << 30,
-             stream=None)
+             hkv=2, d=128, causal=1, scale=0.1, dq=FAKE, dk=FAKE, dv=FAKE, acc=0, ws=FAKE,
+             wsb=1 << 30, stream=None)
     a.update(kw)
     return P.lib().attn_bwd_chunk(a["q"], a["k"], a["v"], a["o"], a["lse"], a["do"], a["tq"],
                                   a["tk"], a["qo"], a["ko"], a["hq"], a["hkv"], a["d"],
-                                  a["causal"], a["scale"], a["dq"], a["dk"], a["dv"], a["ws"],
-                                  a["wsb"], a["stream"])
+                                  a["causal"], a["scale"], a["dq"], a["dk"], a["dv"], a["acc"],
+                                  a["ws"], a["wsb"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,status,msg", [
@@ -154,6 +154,7 @@ def test_fwd_chunk_argument_errors(kw, status, msg):
     (dict(dv=0), P.PDY_ERR_INVALID_ARG, "dv is NULL"),
     (dict(lse=FAKE + 4), P.PDY_ERR_INVALID_ARG, "aligned"),
     (dict(wsb=64), P.PDY_ERR_WORKSPACE, "attn_bwd_chunk"),
+    (dict(acc=2), P.PDY_ERR_INVALID_ARG, "accumulate"),
 ])
 def test_bwd_chunk_argument_errors(kw, status, msg):
     st = _bwd_chunk(**kw)
