@@ -1,102 +1,319 @@
-"""Context-parallel (sequence-sharded) attention: one device's ring steps,
-and the whole ring run on one GPU.
+"""Context-parallel (sequence-sharded) attention: the ring steps of each
+device, run one device after another on a single GPU.
 
-With p devices, device r holds chunk r of the sequence (queries, keys and
-values of positions chunk_bounds[r]).  Key/value chunks travel around the
-ring, so at step t device r holds chunk (r - t) mod p (section 2.2: the
-context-parallel strategies exchange K/V between sequence chunks).  Per step
-the device calls attn_fwd_chunk and folds the partial result into its
-running (O, LSE) with attn_merge.  The backward, given the final O and LSE,
-calls attn_bwd_chunk per step, accumulating dQ of its own chunk and the dK/dV
-of the visiting chunk, which travel on with it.  Under a causal mask a chunk
-after the device's own contributes nothing and is skipped.
+With p devices every device owns some query positions of the sequence and
+the keys/values of the same positions (section 2.2: the context-parallel
+strategies shard the sequence and exchange K/V between the shards).  Two
+layouts:
 
-ring_forward / ring_backward run all devices' steps one after another on a
-single GPU (the exchanges become no-ops): a single-GPU check of the chunked
-path against plain attention, and a measure of its throughput.  Every step
-runs in the library's kernels; this module only orders the calls.
+* contiguous: device r owns chunk r of p near-equal chunks;
+* zigzag: the sequence is cut into 2p chunks and device r owns chunks r and
+  2p-1-r, which evens out the causal work (an early chunk sees few keys, its
+  partner near the end sees many).
+
+Key/value shards travel around the ring, so at step t device r holds the
+shard of device (r - t) mod p.  For every (own query range, visiting key
+range) pair with at least one visible key the device calls attn_fwd_chunk
+and folds the partial result into that range's running (O, LSE) with
+attn_merge.  The backward, given the final O and LSE, calls attn_bwd_chunk
+per pair, accumulating dQ of its own ranges and dK/dV of the visiting shard,
+which travel on with it.  At step 0 a device's diagonal pairs run first and
+overwrite, so each of its dQ and dK/dV buffers is written before anything
+is added to it; every later call adds.
+
+ring_forward / ring_backward run the devices' steps one after another on one
+GPU (the exchanges become no-ops): a single-GPU check of the chunked path
+against plain attention.  `python -m paper_2511_13198_amd.context_parallel`
+times each device's share of a ring (its forward and backward calls) at a
+full sequence length.  Every step runs in the library's kernels; this module
+only orders the calls.
 """
 from __future__ import annotations
 
-from typing import List, Optional, Sequence, Tuple
+import argparse
+import json
+import sys
+import time
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
 
 from . import pdyattn
 
+Range = Tuple[int, int]
 
-def chunk_bounds(total_tokens: int, p: int) -> List[Tuple[int, int]]:
-    """p contiguous chunks of near-equal length (the first T mod p one longer)."""
-    if p < 1:
-        raise ValueError("p must be >= 1")
-    base, extra = divmod(total_tokens, p)
+
+def chunk_bounds(total_tokens: int, n: int) -> List[Range]:
+    """n contiguous chunks of near-equal length (the first T mod n one longer)."""
+    if n < 1:
+        raise ValueError("the number of chunks must be >= 1")
+    base, extra = divmod(total_tokens, n)
     out, a = [], 0
-    for r in range(p):
+    for r in range(n):
         b = a + base + (1 if r < extra else 0)
         out.append((a, b))
         a = b
     return out
 
 
-def _visible(qa: int, qb: int, ka: int, kb: int, causal: bool) -> bool:
-    """Whether any key of [ka, kb) is visible to a query of [qa, qb)."""
-    return qb > qa and kb > ka and (not causal or ka <= qb - 1)
+def device_ranges(total_tokens: int, p: int, layout: str = "contiguous") -> List[List[Range]]:
+    """Position ranges owned by each of the p devices, in position order."""
+    if layout == "contiguous":
+        return [[c] for c in chunk_bounds(total_tokens, p)]
+    if layout == "zigzag":
+        c = chunk_bounds(total_tokens, 2 * p)
+        return [[c[r], c[2 * p - 1 - r]] for r in range(p)]
+    raise ValueError(f"unknown layout {layout!r}")
 
 
 def ring_order(r: int, p: int) -> List[int]:
-    """Key/value chunk held by device r at steps 0 .. p-1."""
+    """Device whose key/value shard device r holds at steps 0 .. p-1."""
     return [(r - t) % p for t in range(p)]
 
 
-def ring_forward(q, k, v, p: int, causal: bool = True, scale: Optional[float] = None):
-    """O [T, Hq, d] and the per-chunk LSE list ([Hq, len_r] each) of the
-    sequence, computed chunk by chunk in ring order."""
+def visible(q: Range, k: Range, causal: bool) -> bool:
+    """Whether any key of range k is visible to a query of range q."""
+    (qa, qb), (ka, kb) = q, k
+    return qb > qa and kb > ka and (not causal or ka <= qb - 1)
+
+
+def pair_count(q: Range, k: Range, causal: bool) -> int:
+    """Number of (query, key) pairs of the two ranges that attend (per head)."""
+    (qa, qb), (ka, kb) = q, k
+    if qb <= qa or kb <= ka:
+        return 0
+    if not causal:
+        return (qb - qa) * (kb - ka)
+
+    def upto(n: int) -> int:
+        # sum over query positions i < n of min(max(i - ka + 1, 0), kb - ka)
+        if n <= ka:
+            return 0
+        ramp_end = min(n, kb)                   # i in [ka, ramp_end): i - ka + 1 keys
+        m = ramp_end - ka
+        return m * (m + 1) // 2 + max(0, n - kb) * (kb - ka)
+
+    return upto(qb) - upto(qa)
+
+
+def device_steps(r: int, ranges: Sequence[Sequence[Range]], causal: bool
+                 ) -> List[Tuple[Range, Range, bool]]:
+    """Chunk pairs of device r in call order: (query range, key range,
+    accumulate).  Step 0 (its own shard) puts the diagonal pairs first; they
+    are called even when empty so that every output buffer gets written."""
+    p = len(ranges)
+    own = ranges[r]
+    out: List[Tuple[Range, Range, bool]] = [(rg, rg, False) for rg in own]
+    for q in own:
+        for k in own:
+            if q != k and visible(q, k, causal):
+                out.append((q, k, True))
+    for src in ring_order(r, p)[1:]:
+        for k in ranges[src]:
+            for q in own:
+                if visible(q, k, causal):
+                    out.append((q, k, True))
+    return out
+
+
+def device_pairs(r: int, ranges: Sequence[Sequence[Range]], causal: bool) -> int:
+    return sum(pair_count(q, k, causal) for q, k, _ in device_steps(r, ranges, causal))
+
+
+def ring_forward(q, k, v, p: int, causal: bool = True, scale: Optional[float] = None,
+                 layout: str = "contiguous", devices: Optional[Iterable[int]] = None,
+                 out=None):
+    """O [T, Hq, d] and {query range: LSE [Hq, len]} of the sequence, computed
+    range pair by range pair in each device's ring order.  `devices` limits
+    the work to those devices' query ranges (the rest of O is left as is)."""
     import torch
-    T = q.shape[0]
-    bounds = chunk_bounds(T, p)
-    o = torch.empty_like(q)
-    lses = []
-    for r, (qa, qb) in enumerate(bounds):
-        acc = None
-        for src in ring_order(r, p):
-            ka, kb = bounds[src]
-            if not _visible(qa, qb, ka, kb, causal):
+    ranges = device_ranges(q.shape[0], p, layout)
+    o = torch.empty_like(q) if out is None else out
+    lses: Dict[Range, object] = {}
+    for r in (range(p) if devices is None else devices):
+        acc: Dict[Range, tuple] = {}
+        for (qa, qb), (ka, kb), _ in device_steps(r, ranges, causal):
+            if (qa, qb) not in acc:
+                acc[(qa, qb)] = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka,
+                                                       causal, scale, out=o[qa:qb])
                 continue
-            if acc is None:
-                acc = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka, causal, scale,
-                                             out=o[qa:qb])
-            else:
-                part = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka, causal,
-                                              scale)
-                acc = pdyattn.attn_merge(acc[0], acc[1], part[0], part[1], out=acc[0],
-                                         lse=acc[1])
-        if acc is None:  # an empty chunk
-            acc = pdyattn.attn_fwd_chunk(q[qa:qb], k[qa:qa], v[qa:qa], qa, qa, causal, scale,
-                                         out=o[qa:qb])
-        lses.append(acc[1])
+            part = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka, causal, scale)
+            ao, al = acc[(qa, qb)]
+            acc[(qa, qb)] = pdyattn.attn_merge(ao, al, part[0], part[1], out=ao, lse=al)
+        for rg, (_, l) in acc.items():
+            lses[rg] = l
     return o, lses
 
 
-def ring_backward(q, k, v, o, lses: Sequence, dout, p: int, causal: bool = True,
-                  scale: Optional[float] = None):
-    """dQ [T, Hq, d], dK and dV [T, Hkv, d] (fp32) from the chunk pairs in
-    ring order, accumulated in the kernels."""
+def ring_backward(q, k, v, o, lses: Dict[Range, object], dout, p: int, causal: bool = True,
+                  scale: Optional[float] = None, layout: str = "contiguous",
+                  devices: Optional[Iterable[int]] = None, grads=None):
+    """dQ [T, Hq, d], dK and dV [T, Hkv, d] (fp32) accumulated in the kernels
+    over the range pairs, ring step by ring step.  With `devices` only those
+    devices' calls run; a visiting shard's dK/dV then has to arrive in
+    `grads` already holding the earlier devices' sums (zero for a timing)."""
     import torch
     T, hq, d = q.shape
     hkv = k.shape[1]
-    bounds = chunk_bounds(T, p)
-    dq = torch.empty((T, hq, d), dtype=torch.float32, device=q.device)
-    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
-    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
-    kv_started = [False] * p
-    # every chunk's own (diagonal) pair comes first at step 0, so each dK/dV
-    # chunk is written before anything is added to it
-    for t in range(p):
-        for r, (qa, qb) in enumerate(bounds):
-            src = ring_order(r, p)[t]
-            ka, kb = bounds[src]
-            if t > 0 and not _visible(qa, qb, ka, kb, causal):
-                continue
-            pdyattn.attn_bwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], o[qa:qb], lses[r], dout[qa:qb],
-                                   qa, ka, causal, scale, dq=dq[qa:qb], dk=dk[ka:kb],
-                                   dv=dv[ka:kb], accumulate=(t > 0 or kv_started[src]))
-            kv_started[src] = True
+    ranges = device_ranges(T, p, layout)
+    if grads is None:
+        grads = (torch.empty((T, hq, d), dtype=torch.float32, device=q.device),
+                 torch.empty((T, hkv, d), dtype=torch.float32, device=q.device),
+                 torch.empty((T, hkv, d), dtype=torch.float32, device=q.device))
+    dq, dk, dv = grads
+    devs = list(range(p) if devices is None else devices)
+    steps = {r: device_steps(r, ranges, causal) for r in devs}
+    # step 0 of every device before any later step: each shard's own device
+    # overwrites its dK/dV before other devices add to it
+    n_own = {r: sum(1 for _, _, acc in steps[r] if not acc) for r in devs}
+    for phase in (0, 1):
+        for r in devs:
+            calls = steps[r][:n_own[r]] if phase == 0 else steps[r][n_own[r]:]
+            for (qa, qb), (ka, kb), accumulate in calls:
+                pdyattn.attn_bwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], o[qa:qb], lses[(qa, qb)],
+                                       dout[qa:qb], qa, ka, causal, scale, dq=dq[qa:qb],
+                                       dk=dk[ka:kb], dv=dv[ka:kb], accumulate=accumulate)
     return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# Timing of one device's share
+# ---------------------------------------------------------------------------
+def time_device(inputs: dict, r: int, p: int, layout: str, causal: bool, reps: int,
+                warmup: int, o, lses_all, grads) -> Tuple[float, float]:
+    """Mean (forward ms, backward ms) of device r's calls over `reps` runs."""
+    import torch
+    q, k, v, do = inputs["q"], inputs["k"], inputs["v"], inputs["do"]
+    fwd, bwd = [], []
+    for it in range(warmup + reps):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        _, lses = ring_forward(q, k, v, p, causal, layout=layout, devices=[r], out=o)
+        e1.record()
+        lses_all.update(lses)
+        ring_backward(q, k, v, o, lses_all, do, p, causal, layout=layout, devices=[r],
+                      grads=grads)
+        e2.record()
+        torch.cuda.synchronize()
+        if it >= warmup:
+            fwd.append(e0.elapsed_time(e1))
+            bwd.append(e1.elapsed_time(e2))
+    return sum(fwd) / len(fwd), sum(bwd) / len(bwd)
+
+
+def measure(tokens: int, p: int, hq: int, hkv: int, d: int, layouts: Sequence[str],
+            causal: bool, reps: int, warmup: int, seed: int = 42) -> dict:
+    """Per-device times of each layout plus the unsharded kernels' time, all at
+    the same sequence.  Dk/dV/dQ buffers are zeroed outside the timed region
+    (a visiting shard's partial sums arrive with it)."""
+    import torch
+    from . import accounting as acc
+    from .workloads import device_inputs
+    inputs = device_inputs(tokens, hq, hkv, d, seed=seed)
+    q = inputs["q"]
+    o = torch.empty_like(q)
+    grads = (torch.zeros((tokens, hq, d), dtype=torch.float32, device=q.device),
+             torch.zeros((tokens, hkv, d), dtype=torch.float32, device=q.device),
+             torch.zeros((tokens, hkv, d), dtype=torch.float32, device=q.device))
+    rec = {"tokens": tokens, "p": p, "heads_q": hq, "heads_kv": hkv, "head_dim": d,
+           "causal": causal, "reps": reps, "warmup": warmup,
+           "flops_per_pair": 14.0 * d * hq, "layouts": {}}
+    # the unsharded step at the same length, for reference
+    cu = torch.tensor([0, tokens], dtype=torch.int32, device=q.device)
+    times = []
+    for it in range(warmup + reps):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        out, lse = pdyattn.attn_fwd(q, inputs["k"], inputs["v"], cu, tokens, causal)
+        e1.record()
+        pdyattn.attn_bwd(q, inputs["k"], inputs["v"], out, lse, inputs["do"], cu, tokens, causal)
+        e2.record()
+        torch.cuda.synchronize()
+        if it >= warmup:
+            times.append((e0.elapsed_time(e1), e1.elapsed_time(e2)))
+    del out, lse
+    f, b = (sum(x) / len(x) for x in zip(*times))
+    full_pairs = acc.pairs_per_head([tokens], causal)
+    rec["unsharded"] = {"fwd_ms": f, "bwd_ms": b, "pairs_per_head": full_pairs,
+                        "tflops": rec["flops_per_pair"] * full_pairs / ((f + b) * 1e9)}
+    print(f"unsharded T={tokens}: fwd {f:.2f} ms bwd {b:.2f} ms "
+          f"{rec['unsharded']['tflops']:.1f} TFLOP/s", flush=True)
+    for layout in layouts:
+        ranges = device_ranges(tokens, p, layout)
+        devs = []
+        lses_all: Dict[Range, object] = {}
+        for r in range(p):
+            f, b = time_device(inputs, r, p, layout, causal, reps, warmup, o, lses_all, grads)
+            pairs = device_pairs(r, ranges, causal)
+            n_calls = len(device_steps(r, ranges, causal))
+            devs.append({"device": r, "ranges": ranges[r], "calls": n_calls,
+                         "pairs_per_head": pairs, "fwd_ms": f, "bwd_ms": b,
+                         "tflops": rec["flops_per_pair"] * pairs / ((f + b) * 1e9)})
+            print(f"{layout} device {r}: {n_calls} pair calls, fwd {f:.2f} ms bwd {b:.2f} ms "
+                  f"{devs[-1]['tflops']:.1f} TFLOP/s", flush=True)
+        slowest = max(x["fwd_ms"] + x["bwd_ms"] for x in devs)
+        rec["layouts"][layout] = {
+            "devices": devs, "step_ms": slowest,
+            "imbalance": slowest / (sum(x["fwd_ms"] + x["bwd_ms"] for x in devs) / p),
+            "speedup_vs_unsharded": (rec["unsharded"]["fwd_ms"] + rec["unsharded"]["bwd_ms"])
+            / slowest}
+    return rec
+
+
+def markdown(rec: dict, command: str) -> str:
+    u = rec["unsharded"]
+    lines = [f"# Context-parallel ring, one device's share: T={rec['tokens']}, p={rec['p']}, "
+             f"Hq={rec['heads_q']}, Hkv={rec['heads_kv']}, d={rec['head_dim']}, "
+             f"causal={rec['causal']}, MI355X", "",
+             f"Command: `{command}`", "",
+             "Each device's forward (chunk calls + merges) and backward (chunk calls with "
+             "accumulation) timed with events, mean of "
+             f"{rec['reps']} runs after {rec['warmup']} warm-up runs; exchanges are not "
+             "modelled (a shard is already resident when its step starts).  TFLOP/s counts "
+             "14 d Hq FLOPs per attending (query, key) pair.", "",
+             f"Unsharded attn_fwd + attn_bwd at the same length: {u['fwd_ms']:.1f} + "
+             f"{u['bwd_ms']:.1f} ms, {u['tflops']:.1f} TFLOP/s.", ""]
+    for layout, L in rec["layouts"].items():
+        lines += [f"## Layout {layout}: slowest device {L['step_ms']:.1f} ms, imbalance "
+                  f"(slowest / mean) {L['imbalance']:.3f}, {L['speedup_vs_unsharded']:.2f}x the "
+                  "unsharded step", "",
+                  "| device | ranges | pair calls | pairs per head | fwd ms | bwd ms | TFLOP/s |",
+                  "|---|---|---|---|---|---|---|"]
+        for x in L["devices"]:
+            rg = ", ".join(f"[{a}, {b})" for a, b in x["ranges"])
+            lines.append(f"| {x['device']} | {rg} | {x['calls']} | {x['pairs_per_head']} | "
+                         f"{x['fwd_ms']:.2f} | {x['bwd_ms']:.2f} | {x['tflops']:.1f} |")
+        lines.append("")
+    return "\n".join(lines)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description="time each device's share of a context-parallel ring")
+    ap.add_argument("--tokens", type=int, default=638976)
+    ap.add_argument("--p", type=int, default=8)
+    ap.add_argument("--heads-q", type=int, default=4)
+    ap.add_argument("--heads-kv", type=int, default=4)
+    ap.add_argument("--head-dim", type=int, default=128)
+    ap.add_argument("--layouts", default="contiguous,zigzag")
+    ap.add_argument("--non-causal", action="store_true")
+    ap.add_argument("--reps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--md")
+    ap.add_argument("--json")
+    a = ap.parse_args(argv)
+    t0 = time.time()
+    rec = measure(a.tokens, a.p, a.heads_q, a.heads_kv, a.head_dim, a.layouts.split(","),
+                  not a.non_causal, a.reps, a.warmup)
+    cmd = "python -m paper_2511_13198_amd.context_parallel " + " ".join(
+        argv if argv is not None else sys.argv[1:])
+    md = markdown(rec, cmd)
+    if a.md:
+        open(a.md, "w").write(md + "\n")
+    else:
+        print(md)
+    if a.json:
+        with open(a.json, "w") as fh:
+            json.dump(rec, fh, indent=1)
+    print(f"done in {time.time() - t0:.0f} s", flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -12,12 +12,7 @@ from tests.parity_util import check_close, log, to_device_bf16
 pytestmark = pytest.mark.gpu
 
 
-def test_chunk_bounds():
-    assert cp.chunk_bounds(10, 3) == [(0, 4), (4, 7), (7, 10)]
-    assert cp.chunk_bounds(2, 4) == [(0, 1), (1, 2), (2, 2), (2, 2)]
-    assert cp.ring_order(1, 4) == [1, 0, 3, 2]
-
-
+@pytest.mark.parametrize("layout", ["contiguous", "zigzag"])
 @pytest.mark.parametrize("T,hq,hkv,d,causal,p", [
     (1500, 4, 2, 128, True, 3),
     (1024, 2, 2, 64, True, 4),
@@ -25,19 +20,19 @@ def test_chunk_bounds():
     (700, 2, 2, 128, False, 2),
     (3, 1, 1, 128, True, 5),      # more devices than tokens: empty chunks
 ])
-def test_ring_matches_full_attention(T, hq, hkv, d, causal, p):
+def test_ring_matches_full_attention(T, hq, hkv, d, causal, p, layout):
     import torch
     bits = wl.host_inputs(T, hq, hkv, d, seed=17)
     f = {n: wl.bf16_bits_to_f64(b) for n, b in bits.items()}
     scale = 1.0 / np.sqrt(d)
-    log(f"  ring p={p} T={T} Hq={hq} Hkv={hkv} d={d} causal={causal}")
+    log(f"  ring {layout} p={p} T={T} Hq={hq} Hkv={hkv} d={d} causal={causal}")
     O, L, dQ, dK, dV = ora.backward(f["q"], f["k"], f["v"], f["do"], np.array([0, T]), causal,
                                     scale)
     q, k, v, do = (to_device_bf16(bits[n]) for n in ("q", "k", "v", "do"))
-    o, lses = cp.ring_forward(q, k, v, p, causal, scale)
-    dq, dk, dv = cp.ring_backward(q, k, v, o, lses, do, p, causal, scale)
+    o, lses = cp.ring_forward(q, k, v, p, causal, scale, layout=layout)
+    dq, dk, dv = cp.ring_backward(q, k, v, o, lses, do, p, causal, scale, layout=layout)
     torch.cuda.synchronize()
-    lse = np.concatenate([x.cpu().numpy() for x in lses], axis=1)
+    lse = np.concatenate([lses[rg].cpu().numpy() for rg in sorted(lses)], axis=1)
     check_close("O", o.double().cpu().numpy(), O)
     check_close("LSE", lse, L)
     check_close("dQ", dq.double().cpu().numpy(), dQ)
