@@ -192,7 +192,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int q_tr = tr_lane_base<QL>();
   const int k_row = row_lane_base<KL>();
 
-  auto compute = [&](int step) __attribute__((always_inline)) {
+  // returns false for a wave with nothing to do in this step; `hook(KS)` runs
+  // after the products of K-step KS of S/dP (active waves only)
+  auto compute = [&](int step, auto&& hook) __attribute__((always_inline)) {
     const int b = step & 1;
     const uint16_t* qs = qbuf(b);
     const uint16_t* gs = gbuf(b);
@@ -200,7 +202,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     const float* dd_s = lse_s + BQ;
     const int wr0 = qstart + (step % nqt) * BQ + half * 32;  // first row of this wave
     const bool active = (kw0 < k_hi) && (wr0 < q_hi) && (!a.causal || wr0 + 31 + shift >= kw0);
-    if (!active) return;
+    if (!active) return false;
     const bool need_mask = (a.causal && wr0 + shift < kw0 + 31) || (wr0 + 32 > q_hi);
     // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows;
     // the four operand fragments of a K-step are read PIPE steps ahead
@@ -230,6 +232,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
         }
         s = mfma32(as_bf16x8(rq[sl]), as_bf16x8(rk[sl]), s);
         dp = mfma32(as_bf16x8(rg[sl]), as_bf16x8(rv[sl]), dp);
+        hook(KS);
       });
     }
     if (need_mask) {  // diagonal or segment-end step only
@@ -279,7 +282,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     tr_wait<0>(rb);
 #pragma unroll
     for (int db = 0; db < NDB; ++db) dka[db] = mfma32(rb[db].operand(), sb1, dka[db]);
+    return true;
   };
+  auto no_hook = [](auto) {};
 
   auto row_ptr = [&](const uint16_t* t, int step) __attribute__((always_inline)) {
     const int h = hk * g + step / nqt;
@@ -300,7 +305,10 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       kvd.issue(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, ktile_s);
       kvd.issue(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, vtile);
     }
-    TileDma<QL, BQ, NW> qd;
+    using QD = TileDma<QL, BQ, NW>;
+    constexpr int PQ = QD::PER_WAVE;  // copies of one tile per wave (at most)
+    static_assert(2 * PQ <= D / 16, "one copy per K-step of S/dP");
+    QD qd;
     qd.init(qstride);
     auto issue = [&](int step) __attribute__((always_inline)) {
       qd.issue(row_ptr(a.q, step), qstride, rows_valid(step), qbuf(step & 1));
@@ -309,18 +317,30 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     if (nsteps > 0) {
       issue(0);
       load_stat(0);
-      store_stat(0);
     }
     for (int step = 0; step < nsteps; ++step) {
       const bool more = step + 1 < nsteps;
+      // this step's tiles and statistics have landed (they were issued
+      // during the previous step); the statistics go to LDS before the barrier
       wait_dma();
+      store_stat(step & 1);
       __syncthreads();
-      if (more) {
-        issue(step + 1);
-        load_stat(step + 1);
-      }
-      compute(step);
-      if (more) store_stat((step + 1) & 1);
+      if (more) load_stat(step + 1);
+      // the next step's copies go out one per K-step of S/dP, so that they
+      // trickle into the memory pipeline instead of stalling every wave at once
+      const uint16_t* qn = row_ptr(a.q, step + 1);
+      const uint16_t* gn = row_ptr(a.dout, step + 1);
+      const int rvn = rows_valid(step + 1);
+      const int bn = (step + 1) & 1;
+      const bool ran = compute(step, [&](auto KS) __attribute__((always_inline)) {
+        constexpr int c = decltype(KS)::value;
+        if constexpr (c < PQ) {
+          if (more) qd.template issue_one<c>(qn, qstride, rvn, qbuf(bn));
+        } else if constexpr (c < 2 * PQ) {
+          if (more) qd.template issue_one<c - PQ>(gn, qstride, rvn, gbuf(bn));
+        }
+      });
+      if (!ran && more) issue(step + 1);
     }
   } else {
     {
@@ -349,7 +369,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       const bool more = step + 1 < nsteps;
       if (more) issue(step + 1);
       __syncthreads();
-      compute(step);
+      compute(step, no_hook);
       if (more) commit((step + 1) & 1);
     }
   }

@@ -299,8 +299,9 @@ struct TileLoader {
 // store instructions) of a [ROWS x 128] bf16 tile into layout L.  One
 // instruction moves 64 lanes x 16 B into 1 KB of consecutive LDS (lane l at
 // base + 16 l); lane l of instruction k therefore fills 16-byte slot 64 k + l
-// of the tile and fetches whichever global chunk the layout stores there
-// (padding slots re-read a valid chunk).  Rows >= valid_rows repeat the last
+// of the tile and fetches whichever global chunk the layout stores there;
+// the lanes of padding slots are switched off, so padding costs no memory
+// traffic (its LDS bytes are never read).  Rows >= valid_rows repeat the last
 // valid row; callers mask them.  Completion is tracked by vmcnt (wait_dma).
 template <class L, int ROWS, int NW>
 struct TileDma {
@@ -310,7 +311,7 @@ struct TileDma {
   static_assert(SLOTS % 64 == 0, "tile must fill whole 1 KB copies");
   uint32_t goff[PER_WAVE];  // byte offset of this lane's chunk in each copy, full tiles
   int srow[PER_WAVE];       // tile row, for clamping at a segment end
-  int schunk[PER_WAVE];
+  int schunk[PER_WAVE];      // chunk within the row, -1 for a padding slot
 
   __device__ __forceinline__ void init(size_t gstride) {
     const int l = __lane_id();
@@ -319,11 +320,10 @@ struct TileDma {
     for (int i = 0; i < PER_WAVE; ++i) {
       const int slot = (w + NW * i) * 64 + l;
       const int r = slot / L::SLOTS_PER_ROW;
-      int c = L::chunk_at(r, slot % L::SLOTS_PER_ROW);
-      c = c < 0 ? 0 : c;
+      const int c = L::chunk_at(r, slot % L::SLOTS_PER_ROW);
       srow[i] = r;
       schunk[i] = c;
-      goff[i] = (uint32_t)(((size_t)r * gstride + (size_t)c * 8) * 2);
+      goff[i] = (uint32_t)(((size_t)r * gstride + (size_t)(c < 0 ? 0 : c) * 8) * 2);
     }
   }
   // Copy I of this wave alone (I < PER_WAVE); a no-op where the wave has no
@@ -341,9 +341,10 @@ struct TileDma {
       const int rr = srow[I] < valid_rows ? srow[I] : valid_rows - 1;
       off = (uint32_t)(((size_t)rr * gstride + (size_t)schunk[I] * 8) * 2);
     }
-    __builtin_amdgcn_global_load_lds(
-        (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
-        (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
+    if (schunk[I] >= 0)
+      __builtin_amdgcn_global_load_lds(
+          (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
+          (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
   }
   __device__ __forceinline__ void issue(const uint16_t* gbase, size_t gstride, int valid_rows,
                                         uint16_t* lds) const {
@@ -358,9 +359,10 @@ struct TileDma {
         const int rr = srow[i] < valid_rows ? srow[i] : valid_rows - 1;
         off = (uint32_t)(((size_t)rr * gstride + (size_t)schunk[i] * 8) * 2);
       }
-      __builtin_amdgcn_global_load_lds(
-          (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
-          (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
+      if (schunk[i] >= 0)
+        __builtin_amdgcn_global_load_lds(
+            (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
+            (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
     }
   }
 };
