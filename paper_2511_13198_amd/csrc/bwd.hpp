@@ -295,9 +295,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     return q_hi - (qstart + (step % nqt) * BQ);
   };
 
-  // K and V tiles (keys past the segment end repeat the last key; their
-  // gradients are never written out); query-side tiles repeat the last row
-  // past the segment end and are masked.
+  // K and V tiles: keys past the segment end read as zeros (d = 128 copies)
+  // or repeat the last key (d = 64 loads); their gradients are never written
+  // out.  Query-side rows past the segment end likewise, and are masked.
   if constexpr (D == 128) {
     {
       TileDma<KL, BK, NW> kvd;
@@ -328,16 +328,17 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       if (more) load_stat(step + 1);
       // the next step's copies go out one per K-step of S/dP, so that they
       // trickle into the memory pipeline instead of stalling every wave at once
-      const uint16_t* qn = row_ptr(a.q, step + 1);
-      const uint16_t* gn = row_ptr(a.dout, step + 1);
+      // (built for every step; only used when there is a next one)
       const int rvn = rows_valid(step + 1);
+      const typename QD::Src rsq = QD::src(row_ptr(a.q, step + 1), qstride, rvn);
+      const typename QD::Src rsg = QD::src(row_ptr(a.dout, step + 1), qstride, rvn);
       const int bn = (step + 1) & 1;
       const bool ran = compute(step, [&](auto KS) __attribute__((always_inline)) {
         constexpr int c = decltype(KS)::value;
         if constexpr (c < PQ) {
-          if (more) qd.template issue_one<c>(qn, qstride, rvn, qbuf(bn));
+          if (more) qd.issue_one(c, rsq, qbuf(bn));
         } else if constexpr (c < 2 * PQ) {
-          if (more) qd.template issue_one<c - PQ>(gn, qstride, rvn, gbuf(bn));
+          if (more) qd.issue_one(c - PQ, rsg, gbuf(bn));
         }
       });
       if (!ran && more) issue(step + 1);
@@ -554,7 +555,8 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
     });
   };
 
-  // rows past the segment end repeat the last key; they are always masked
+  // keys past the segment end read as zeros (d = 128 copies) or repeat the
+  // last key (d = 64 loads); they are always masked
   if constexpr (D == 128) {
     TileDma<KL, BK, NW> kd;
     TileDma<VL, BK, NW> vd;

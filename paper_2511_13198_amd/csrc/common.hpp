@@ -20,6 +20,10 @@
 
 namespace pdy {
 
+// Fourth word of a raw buffer resource on gfx950 (32-bit data format, no
+// swizzle): the value the buffer range check and LDS copies were verified with.
+constexpr int kBufferFlags = 0x00020000;
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -295,74 +299,75 @@ struct TileLoader {
   }
 };
 
-// Direct global -> LDS copy (global_load_lds_dwordx4: no registers, no LDS
+// Direct global -> LDS copy (buffer_load_dwordx4 ... lds: no registers, no LDS
 // store instructions) of a [ROWS x 128] bf16 tile into layout L.  One
 // instruction moves 64 lanes x 16 B into 1 KB of consecutive LDS (lane l at
-// base + 16 l); lane l of instruction k therefore fills 16-byte slot 64 k + l
-// of the tile and fetches whichever global chunk the layout stores there;
-// the lanes of padding slots are switched off, so padding costs no memory
-// traffic (its LDS bytes are never read).  Rows >= valid_rows repeat the last
-// valid row; callers mask them.  Completion is tracked by vmcnt (wait_dma).
+// base + 16 l, the base in M0); lane l of instruction k therefore fills 16-byte
+// slot 64 k + l of the tile and fetches whichever global chunk the layout
+// stores there.  The copies read through a buffer resource over the tile's
+// valid rows: the hardware's range check turns rows >= valid_rows into zeros
+// (callers mask them), and padding slots get an offset past any range, so
+// they fetch nothing.  Per copy this leaves one M0 write and the load, with
+// the lane offsets computed once.  Completion is tracked by vmcnt (wait_dma).
 template <class L, int ROWS, int NW>
 struct TileDma {
   static constexpr int SLOTS = ROWS * L::SLOTS_PER_ROW;
   static constexpr int INSTS = SLOTS / 64;
   static constexpr int PER_WAVE = (INSTS + NW - 1) / NW;
   static_assert(SLOTS % 64 == 0, "tile must fill whole 1 KB copies");
-  uint32_t goff[PER_WAVE];  // byte offset of this lane's chunk in each copy, full tiles
-  int srow[PER_WAVE];       // tile row, for clamping at a segment end
-  int schunk[PER_WAVE];      // chunk within the row, -1 for a padding slot
+  static constexpr uint32_t kPadOffset = 0x80000000u;  // out of range for every tile
+  uint32_t voff[PER_WAVE];  // byte offset of this lane's chunk in each copy
+  int wave;                 // this wave's index (wave-uniform)
 
   __device__ __forceinline__ void init(size_t gstride) {
     const int l = __lane_id();
-    const int w = threadIdx.x >> 6;
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i) {
-      const int slot = (w + NW * i) * 64 + l;
+      const int slot = (wave + NW * i) * 64 + l;
       const int r = slot / L::SLOTS_PER_ROW;
       const int c = L::chunk_at(r, slot % L::SLOTS_PER_ROW);
-      srow[i] = r;
-      schunk[i] = c;
-      goff[i] = (uint32_t)(((size_t)r * gstride + (size_t)(c < 0 ? 0 : c) * 8) * 2);
+      voff[i] = c < 0 ? kPadOffset : (uint32_t)(((size_t)r * gstride + (size_t)c * 8) * 2);
     }
   }
-  // Copy I of this wave alone (I < PER_WAVE); a no-op where the wave has no
-  // copy I.  Lets a kernel spread its copies over the products of a step
-  // instead of queueing them all at once.
-  template <int I>
-  __device__ __forceinline__ void issue_one(const uint16_t* gbase, size_t gstride, int valid_rows,
-                                            uint16_t* lds) const {
-    static_assert(I < PER_WAVE, "copy index");
-    const int w = threadIdx.x >> 6;
-    const int k = w + NW * I;
+  // Source of one tile: rows [0, min(valid_rows, ROWS)) at gbase.  The
+  // values are wave-uniform; passing them through readfirstlane tells the
+  // compiler so (it would otherwise wrap each copy in a loop over the
+  // distinct values of the lanes).  Built once per tile, used by its copies.
+  struct Src {
+    uint32_t lo, hi;  // address
+    int bytes;        // range of the buffer resource
+  };
+  __device__ __forceinline__ static Src src(const uint16_t* gbase, size_t gstride, int valid_rows) {
+    const int rows = valid_rows < ROWS ? valid_rows : ROWS;
+    const uint64_t addr = reinterpret_cast<uint64_t>(gbase);
+    return {(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)addr),
+            (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(addr >> 32)),
+            (int)__builtin_amdgcn_readfirstlane((int)((size_t)rows * gstride * 2))};
+  }
+  __device__ __forceinline__ static void copy(const Src& s, uint32_t voffset, uint16_t* lds) {
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(((uint64_t)s.hi << 32) | s.lo), 0, s.bytes, kBufferFlags);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16,
+                                             voffset, 0, 0, 0);
+  }
+  // Copy i of this wave alone (0 <= i < PER_WAVE, a constant at the call
+  // site); a no-op where the wave has no copy i.  Lets a kernel spread its
+  // copies over the products of a step instead of queueing them all at once.
+  __device__ __forceinline__ void issue_one(int i, const Src& s, uint16_t* lds) const {
+    const int k = wave + NW * i;
     if (INSTS % NW != 0 && k >= INSTS) return;  // wave-uniform
-    uint32_t off = goff[I];
-    if (valid_rows < ROWS) {
-      const int rr = srow[I] < valid_rows ? srow[I] : valid_rows - 1;
-      off = (uint32_t)(((size_t)rr * gstride + (size_t)schunk[I] * 8) * 2);
-    }
-    if (schunk[I] >= 0)
-      __builtin_amdgcn_global_load_lds(
-          (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
-          (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
+    copy(s, voff[i], lds + k * 512);
   }
+  // All of this wave's copies of the tile (valid_rows >= 1).
   __device__ __forceinline__ void issue(const uint16_t* gbase, size_t gstride, int valid_rows,
                                         uint16_t* lds) const {
-    const int w = threadIdx.x >> 6;
-    const bool full = valid_rows >= ROWS;
+    const Src s = src(gbase, gstride, valid_rows);
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i) {
-      const int k = w + NW * i;
+      const int k = wave + NW * i;
       if (INSTS % NW != 0 && k >= INSTS) break;  // wave-uniform
-      uint32_t off = goff[i];
-      if (!full) {
-        const int rr = srow[i] < valid_rows ? srow[i] : valid_rows - 1;
-        off = (uint32_t)(((size_t)rr * gstride + (size_t)schunk[i] * 8) * 2);
-      }
-      if (schunk[i] >= 0)
-        __builtin_amdgcn_global_load_lds(
-            (__attribute__((address_space(1))) void*)(reinterpret_cast<const uint8_t*>(gbase) + off),
-            (__attribute__((address_space(3))) void*)(lds + k * 512), 16, 0, 0);
+      copy(s, voff[i], lds + k * 512);
     }
   }
 };

@@ -243,7 +243,8 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
   auto no_hook = [](auto) {};
-  // rows past the segment end repeat the last key; they are always masked
+  // keys past the segment end read as zeros (d = 128 copies) or repeat the
+  // last key (d = 64 loads); they are always masked
   if constexpr (D == 128) {
     // K/V tiles land in LDS by direct copies, no staging registers
     TileDma<KL, BK, NW> kd;
@@ -273,17 +274,18 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
       if (active(it)) {
         // the copies of tile tn go out one per K-step of S, so that they
         // trickle into the memory pipeline instead of queueing at once
+        // (built for every tile; only used when there is a next one)
         const int kt = k_lo + tn * BK;
-        const uint16_t* kg = kbase + (size_t)kt * kvstride;
-        const uint16_t* vg = vbase + (size_t)kt * kvstride;
+        const auto rsk = TileDma<KL, BK, NW>::src(kbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
+        const auto rsv = TileDma<VL, BK, NW>::src(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
         uint16_t* kl = kbuf(tn);
         uint16_t* vl = vbuf(tn);
         auto copy = [&](auto CI) __attribute__((always_inline)) {
           constexpr int c = decltype(CI)::value;
           if constexpr (c < PK) {
-            if (more) kd.template issue_one<c>(kg, kvstride, k_hi - kt, kl);
+            if (more) kd.issue_one(c, rsk, kl);
           } else if constexpr (c < PK + PV) {
-            if (more) vd.template issue_one<c - PK>(vg, kvstride, k_hi - kt, vl);
+            if (more) vd.issue_one(c - PK, rsv, vl);
           }
         };
         // the tile is taken in softmax steps of BKS keys; the first step

@@ -72,6 +72,20 @@ def counters(d: str) -> Dict[str, Dict[str, List[float]]]:
     return {k: {c: list(v.values()) for c, v in cs.items()} for k, cs in out.items()}
 
 
+def clock_ghz(d: str) -> Dict[str, float]:
+    """kernel -> mean shader clock (GHz) over its dispatches in a counter pass
+    with GRBM_GUI_ACTIVE: the counter (summed over the 8 XCDs) / 8 / the
+    dispatch's duration."""
+    per: Dict[str, List[float]] = collections.defaultdict(list)
+    for r in _csv(d, "counter_collection.csv"):
+        if r["Counter_Name"] != "GRBM_GUI_ACTIVE" or not r.get("End_Timestamp"):
+            continue
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+        if dur > 0:
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]) / 8.0 / dur / 1e9)
+    return {k: _mean(v) for k, v in per.items()}
+
+
 def kernel_stats(d: str) -> Dict[str, dict]:
     out = {}
     for r in _csv(d, "kernel_stats.csv"):
@@ -95,6 +109,7 @@ def copy_scale(d: str, counter: str, copy_mib: int) -> float:
 def summarize(a) -> dict:
     stats = kernel_stats(a.trace)
     pmc = counters(a.pmc)
+    clocks = clock_ghz(a.pmc)
     fetch = counters(a.fetch)
     write = counters(a.write)
     fs = copy_scale(a.copy_fetch, "FETCH_SIZE", a.copy_mib)
@@ -112,6 +127,7 @@ def summarize(a) -> dict:
             wave = _mean(p.get("SQ_WAVE_CYCLES", []))
             e["mfma_busy_pct"] = 100.0 * _mean(p.get("SQ_VALU_MFMA_BUSY_CYCLES", [])) / (
                 grbm / 8.0 * 1024.0) if grbm else None
+            e["clock_ghz"] = clocks.get(full)
             for c in ("SQ_ACTIVE_INST_ANY", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
                       "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS"):
                 e[c.lower() + "_pct_of_wave"] = 100.0 * _mean(p.get(c, [])) / wave if wave else None
@@ -129,9 +145,9 @@ def markdown(rec: dict, commands: List[str]) -> str:
     lines += [f"- `{c}`" for c in commands]
     lines += ["", f"Copy calibration: FETCH_SIZE x {rec['fetch_scale']:.3f}, "
               f"WRITE_SIZE x {rec['write_scale']:.3f} (bytes per counter KiB / 1024).", "",
-              "| kernel | calls | avg ms | MFMA busy % | issuing % | waiting (waitcnt/barrier) % "
+              "| kernel | calls | avg ms | clock GHz | MFMA busy % | issuing % | waiting (waitcnt/barrier) % "
               "| waiting to issue % | VALU active % | LDS active % | HBM fetch GB | HBM write GB |",
-              "|---|---|---|---|---|---|---|---|---|---|---|"]
+              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
 
     def f(x, fmt):
         return "" if x is None else format(x, fmt)
@@ -140,7 +156,8 @@ def markdown(rec: dict, commands: List[str]) -> str:
         if not e:
             continue
         lines.append("| " + " | ".join([
-            k, str(e["calls"]), f(e["avg_ms"], ".3f"), f(e.get("mfma_busy_pct"), ".1f"),
+            k, str(e["calls"]), f(e["avg_ms"], ".3f"), f(e.get("clock_ghz"), ".2f"),
+            f(e.get("mfma_busy_pct"), ".1f"),
             f(e.get("sq_active_inst_any_pct_of_wave"), ".1f"),
             f(e.get("sq_wait_any_pct_of_wave"), ".1f"),
             f(e.get("sq_wait_inst_any_pct_of_wave"), ".1f"),
@@ -149,7 +166,10 @@ def markdown(rec: dict, commands: List[str]) -> str:
             f(e.get("fetch_bytes", 0) / 1e9, ".3f"), f(e.get("write_bytes", 0) / 1e9, ".3f"),
         ]) + " |")
     lines += ["", "MFMA busy % = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x 1024 SIMDs); "
-              "the other percentages are of SQ_WAVE_CYCLES (time waves are resident).", ""]
+              "the other percentages are of SQ_WAVE_CYCLES (time waves are resident).  Clock = "
+              "GRBM_GUI_ACTIVE per XCD / dispatch duration in the counter pass (kernels run "
+              "slightly slower under counter collection); the clock-adjusted bf16 peak is "
+              "2516.6 TFLOP/s x clock / 2.4 GHz.", ""]
     return "\n".join(lines)
 
 

@@ -25,14 +25,25 @@ def _counters(d, rows):
                                               "Counter_Value"], rows)
 
 
+def _timed_counters(d, rows):
+    """rows: (dispatch, kernel, counter, value, start_ns, end_ns)"""
+    _write(d, "run_counter_collection.csv", ["Dispatch_Id", "Kernel_Name", "Counter_Name",
+                                              "Counter_Value", "Start_Timestamp",
+                                              "End_Timestamp"], rows)
+
+
 def test_summary_from_fake_rocprof_output(tmp_path):
     t = str(tmp_path)
     _write(t + "/trace", "run_kernel_stats.csv",
            ["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs",
             "StdDev"], [[K, 2, 6e7, 3e7, 100, 2.9e7, 3.1e7, 1]])
-    _counters(t + "/pmc", [[1, K, "GRBM_GUI_ACTIVE", 8 * 1000], [1, K, "SQ_WAVE_CYCLES", 500],
-                           [1, K, "SQ_VALU_MFMA_BUSY_CYCLES", 512 * 1000],
-                           [1, K, "SQ_WAIT_ANY", 100], [1, K, "SQ_ACTIVE_INST_ANY", 250]])
+    # 1000 active cycles per XCD over a 1 us dispatch: a 1 GHz clock
+    ts = [5000, 6000]
+    _timed_counters(t + "/pmc", [[1, K, "GRBM_GUI_ACTIVE", 8 * 1000, *ts],
+                                 [1, K, "SQ_WAVE_CYCLES", 500, *ts],
+                                 [1, K, "SQ_VALU_MFMA_BUSY_CYCLES", 512 * 1000, *ts],
+                                 [1, K, "SQ_WAIT_ANY", 100, *ts],
+                                 [1, K, "SQ_ACTIVE_INST_ANY", 250, *ts]])
     # two dispatches: 100 and 300 KiB fetched; the copy moved 1 MiB and read 512 KiB
     _counters(t + "/fetch", [[1, K, "FETCH_SIZE", 100], [2, K, "FETCH_SIZE", 300]])
     _counters(t + "/write", [[1, K, "WRITE_SIZE", 50], [2, K, "WRITE_SIZE", 50]])
@@ -49,6 +60,7 @@ def test_summary_from_fake_rocprof_output(tmp_path):
     assert e["write_bytes"] == pytest.approx(50 * 1024)
     assert e["mfma_busy_pct"] == pytest.approx(50.0)  # 512000 / (1000 * 1024)
     assert e["sq_wait_any_pct_of_wave"] == pytest.approx(20.0)
+    assert e["clock_ghz"] == pytest.approx(1.0)
     md = pf.markdown(rec, ["cmd one"])
     assert "`cmd one`" in md and "bwd_dkdv_kernel" in md
 
