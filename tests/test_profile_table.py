@@ -102,13 +102,16 @@ def _committed(name):
     return pt.read_csv(os.path.join(os.path.dirname(os.path.dirname(__file__)), "profiles", name))
 
 
-def test_committed_sweep_table_is_consistent():
-    rows = _committed("length_profile_h4_d128.csv")
+@pytest.mark.parametrize("name,hq,hkv", [("length_profile_h4_d128.csv", 4, 4),
+                                          ("length_profile_h32kv8_d128.csv", 32, 8)])
+def test_committed_sweep_table_is_consistent(name, hq, hkv):
+    rows = _committed(name)
     assert [int(r["tokens"]) for r in rows] == pt.sweep_lengths()
     for r in rows:
         s = int(r["tokens"])
         assert int(r["n_seqs"]) == 1 and int(r["max_s"]) == s and int(r["sum_s2"]) == s * s
-        f = acc.fwd_bwd_flops([s], 4, 128)
+        assert (int(r["heads_q"]), int(r["heads_kv"])) == (hq, hkv)
+        f = acc.fwd_bwd_flops([s], hq, 128)
         assert float(r["counted_flops"]) == pytest.approx(f, rel=1e-5)
         assert float(r["fwdbwd_tflops"]) == pytest.approx(
             f / (float(r["fwdbwd_ms"]) * 1e-3) / 1e12, rel=1e-4)
