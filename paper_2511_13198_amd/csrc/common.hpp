@@ -96,9 +96,9 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p, bool valid) {
 // ---------------------------------------------------------------------------
 // LDS tile layouts.  A tile holds rows of D bf16 values as 16-byte chunks; all
 // offsets below are in bf16 elements.  Two access patterns occur:
-//   * row reads (lds_row_operand): a quarter-wave reads the same chunk of 16
+//   * row reads (row_issue): a quarter-wave reads the same chunk of 16
 //     consecutive rows;
-//   * transposing reads (lds_tr_operand): a half-wave reads 4 consecutive rows
+//   * transposing reads (tr_issue): a half-wave reads 4 consecutive rows
 //     x 64 consecutive bytes.
 // RowsLayout pads rows to D + 8 elements (272 B for D = 128), which makes row
 // reads conflict-free.  DualLayout (D = 128) stores row r at 320 r bytes
@@ -159,39 +159,12 @@ __device__ __forceinline__ int tr_lane_base() {
   return L::off(hh * 4 + (i >> 2), g2 * 2 + ((i & 3) >> 1)) + (i & 1) * 4;
 }
 
-// A/B operand whose 8 contraction elements are contiguous in an LDS row:
-// element j of lane l comes from row (row0 + l % 32), column (col0 + (l/32)*8 + j).
-// `lane` = tile + row_lane_base<L>(); row0 % 16 == 0, col0 % 8 == 0 (constants).
-template <class L>
-__device__ __forceinline__ bf16x8 lds_row_operand(const uint16_t* lane, int row0, int col0) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lane + L::delta(row0, col0)));
-}
-
 // A operand "X^T" for an LDS tile X[row][col]: lane l gets
-//   element j = X[row0 + sigma(l/32, j)][col0 + l % 32],  j = 0..7,
+//   element j = X[ROW0 + sigma(l/32, j)][COL0 + l % 32],  j = 0..7,
 // i.e. 8 rows (in sigma order) of one column, with two ds_read_b64_tr_b16
 // (the instruction hands lane i of a 16-lane group element i % 4 of the rows
-// addressed by lanes 4e + i/4, e = 0..3).  `lane` = tile + tr_lane_base<L>();
-// row0 % 16 == 0, col0 % 32 == 0 (constants).
-template <class L>
-__device__ __forceinline__ bf16x8 lds_tr_operand(const uint16_t* lane, int row0, int col0) {
-  const uint16_t* p0 = lane + L::delta(row0, col0);
-  const uint16_t* p1 = p0 + L::TR_P1;
-  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
-  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p1));
-  bf16x4 blo = __builtin_bit_cast(bf16x4, lo);
-  bf16x4 bhi = __builtin_bit_cast(bf16x4, hi);
-  bf16x8 out;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    out[j] = blo[j];
-    out[4 + j] = bhi[j];
-  }
-  return out;
-}
-
-// The same X^T operand, issued with inline assembly so the constant part of
-// the address goes into the instruction's offset field.  (The compiler's
+// addressed by lanes 4e + i/4, e = 0..3), issued with inline assembly so the
+// constant part of the address goes into the instruction's offset field.  (The compiler's
 // intrinsic for this instruction neither folds offsets nor knows it cannot
 // alias in-flight direct-to-LDS copies, and so waits for them.)  The caller
 // must wait with tr_wait before using (or copying) the registers.  `lane_addr` = LDS byte
@@ -245,8 +218,10 @@ __device__ __forceinline__ void tr_wait(TrRegs (&r)[K]) {
   else tr_wait<N>(r[0], r[1]);
 }
 
-// Row-read operand (see lds_row_operand) issued with inline assembly, for
-// explicitly pipelined reads; wait with row_wait before use.  `lane_addr` =
+// A/B operand whose 8 contraction elements are contiguous in an LDS row:
+// element j of lane l comes from row (ROW0 + l % 32), column
+// (COL0 + (l/32)*8 + j); ROW0 % 16 == 0, COL0 % 8 == 0.  Issued with inline
+// assembly for explicitly pipelined reads; wait with row_wait before use.  `lane_addr` =
 // LDS byte address of tile + row_lane_base<L>().
 template <class L, int ROW0, int COL0>
 __device__ __forceinline__ void row_issue(uint32_t lane_addr, u32x4& r) {

@@ -28,6 +28,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 from typing import Dict, List
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -35,13 +36,23 @@ LIBRARY_KERNELS = ("plan_kernel", "fwd_kernel", "bwd_pre_kernel", "bwd_dkdv_kern
                    "bwd_dq_kernel")
 
 
+def code_text(src: str) -> str:
+    """C++ source with comments removed and whitespace collapsed: the part of a
+    kernel source that can change the compiled code.  (String literals in the
+    kernel sources hold no comment markers.)"""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def source_hash() -> str:
-    """sha256 over the HIP sources the library is built from (sorted by name)."""
+    """sha256 over the code (comments and layout aside) of the HIP sources the
+    library is built from, sorted by name."""
     h = hashlib.sha256()
     for p in sorted(glob.glob(os.path.join(_HERE, "csrc", "*"))):
         if p.endswith((".hip", ".hpp", ".h")):
             h.update(os.path.basename(p).encode())
-            h.update(open(p, "rb").read())
+            h.update(code_text(open(p).read()).encode())
     return h.hexdigest()
 
 
@@ -141,7 +152,7 @@ def summarize(a) -> dict:
 
 def markdown(rec: dict, commands: List[str]) -> str:
     lines = [f"# Kernel profile: {rec['workload']}, MI355X", "",
-             f"Kernel sources sha256 `{rec['source_sha256']}`.", "", "Commands:", ""]
+             f"Kernel code sha256 (comments and layout aside) `{rec['source_sha256']}`.", "", "Commands:", ""]
     lines += [f"- `{c}`" for c in commands]
     lines += ["", f"Copy calibration: FETCH_SIZE x {rec['fetch_scale']:.3f}, "
               f"WRITE_SIZE x {rec['write_scale']:.3f} (bytes per counter KiB / 1024).", "",

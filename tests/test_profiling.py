@@ -79,3 +79,11 @@ def test_committed_traffic_record_matches_its_summary():
     assert rec["source_sha256"] in md
     for k in ("fwd_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel"):
         assert rec["kernels"][k]["fetch_bytes"] > 0 and rec["kernels"][k]["write_bytes"] > 0
+
+
+def test_code_text_ignores_comments_and_layout_only():
+    a = "int f(int x) {  // doubles\n  return 2 * x; /* done */\n}\n"
+    b = "int f(int x) {\n    return 2 * x;\n}"
+    c = "int f(int x) { return 3 * x; }"
+    assert pf.code_text(a) == pf.code_text(b)
+    assert pf.code_text(a) != pf.code_text(c)
