@@ -264,6 +264,12 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     const uint32_t ga = lds_addr(gs) + (q_tr + half * 32 * QL::ROW) * 2;
     const uint32_t qa = lds_addr(qs) + (q_tr + half * 32 * QL::ROW) * 2;
     TrRegs ra[NDB], rb[NDB];
+    // the two waves of a SIMD run the same phases at about the same time;
+    // raising the priority of a wave in this product-only phase lets it keep
+    // the matrix core fed while the other wave's exponentials fill the
+    // vector ALU (measured: dK/dV 2% faster; no gain in the other phase or
+    // the other kernels)
+    __builtin_amdgcn_s_setprio(1);
     static_for<NDB>([&](auto DB) { tr_issue<QL, 0, DB * 32>(ga, ra[DB]); });
     static_for<NDB>([&](auto DB) { tr_issue<QL, 0, DB * 32>(qa, rb[DB]); });
     const bf16x8 pb0 = pack8(s, 0), sb0 = pack8(dp, 0);
@@ -282,6 +288,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     tr_wait<0>(rb);
 #pragma unroll
     for (int db = 0; db < NDB; ++db) dka[db] = mfma32(rb[db].operand(), sb1, dka[db]);
+    __builtin_amdgcn_s_setprio(0);
     return true;
   };
   auto no_hook = [](auto) {};
@@ -539,6 +546,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
       // dQ^T += K^T dS^T for the block's two 16-key steps
       constexpr int NDB = D / 32;
       TrRegs kt0[NDB], kt1[NDB];
+      // priority for the wave in this product-only phase, as in the dK/dV
+      // kernel (measured: dQ 2.5% faster)
+      __builtin_amdgcn_s_setprio(1);
       // all of kt0 is issued before kt1, so "at most 2*NDB outstanding" means
       // kt0 has landed
       const uint32_t kab = ka + kb * 32 * KL::ROW * 2;
@@ -552,6 +562,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
       const bf16x8 sb1 = pack8(s, 8);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) dqa[db] = mfma32(kt1[db].operand(), sb1, dqa[db]);
+      __builtin_amdgcn_s_setprio(0);
     });
   };
 
