@@ -167,3 +167,14 @@ def test_stream_batches_gqa():
         _sampled_parity(w, device_gen=True, heads=[0, 17, 31], kv_heads=[0, 7],
                         per_seg_random=4 if w.num_seqs > 1 else 32, tail_cols=64,
                         max_rows=64)
+
+
+def test_stream_longest_batch_gqa():
+    """The 638,976-token batch with 32 query and 8 kv heads: element offsets
+    of q, o and dq pass 2**31."""
+    stream = wl.stream_config5()
+    i = max(range(len(stream)), key=lambda j: stream[j].max_seqlen)
+    w = stream[i]
+    assert w.total_tokens * w.heads_q * w.head_dim > 2 ** 31
+    _sampled_parity(w, device_gen=True, heads=[0, 30], kv_heads=[0, 7], per_seg_random=16,
+                    tail_cols=64, max_rows=48)
