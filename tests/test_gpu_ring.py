@@ -7,7 +7,7 @@ import pytest
 from oracle import attention as ora
 from paper_2511_13198_amd import context_parallel as cp
 from paper_2511_13198_amd import workloads as wl
-from tests.parity_util import check_close, log, to_device_bf16
+from tests.parity_util import HeadView, check_close, log, sample_rows, to_device_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -57,3 +57,48 @@ def test_accumulate_adds_to_what_is_there():
     torch.cuda.synchronize()
     for a, b, fr in zip(acc, base, fresh):
         assert torch.allclose(a, b + fr, rtol=0, atol=1e-5)
+
+
+def test_zigzag_ring_at_131072_tokens():
+    """The p=8 zig-zag ring over one 131,072-token sequence (4 heads, d=128):
+    sampled rows and the last 64 key columns against the oracle, and every
+    element against the unsharded library call (which the single-sequence
+    parity test checks against the oracle at this size), within twice the
+    tolerance since both carry their own rounding."""
+    import torch
+    from paper_2511_13198_amd import pdyattn
+    w = wl.config(3)
+    T, hq, hkv, d = w.total_tokens, w.heads_q, w.heads_kv, w.head_dim
+    scale = w.softmax_scale
+    p = 8
+    log(f"  zig-zag ring p={p} T={T} Hq={hq} d={d}")
+    dev = wl.device_inputs(T, hq, hkv, d)
+    q, k, v, do = dev["q"], dev["k"], dev["v"], dev["do"]
+    o, lses = cp.ring_forward(q, k, v, p, True, scale, layout="zigzag")
+    dq, dk, dv = cp.ring_backward(q, k, v, o, lses, do, p, True, scale, layout="zigzag")
+    lse = torch.empty((hq, T), dtype=torch.float32, device=q.device)
+    for (a, b), l in lses.items():
+        lse[:, a:b] = l
+    cu = torch.tensor([0, T], dtype=torch.int32, device=q.device)
+    o_u, lse_u = pdyattn.attn_fwd(q, k, v, cu, T, True, scale)
+    dq_u, dk_u, dv_u = pdyattn.attn_bwd(q, k, v, o_u, lse_u, do, cu, T, True, scale)
+    torch.cuda.synchronize()
+    for name, g, u in (("O", o, o_u), ("LSE", lse, lse_u), ("dQ", dq, dq_u), ("dK", dk, dk_u),
+                       ("dV", dv, dv_u)):
+        check_close(name + " vs unsharded", g.double().cpu().numpy(), u.double().cpu().numpy(),
+                    max_abs=4e-2, rel_l2=1e-2)
+    host = {n: HeadView(t) for n, t in dev.items()}
+    cu_h = np.array([0, T])
+    rows = sample_rows([T], 24, max_rows=48)
+    res = ora.rows_forward_backward(host["q"], host["k"], host["v"], host["do"], cu_h, True,
+                                    scale, heads=[0, 3], rows=rows)
+    ridx = torch.tensor(rows, dtype=torch.long, device=q.device)
+    for h in (0, 3):
+        check_close("O", o[ridx, h].double().cpu().numpy(), res[h][0])
+        check_close("LSE", lse[h, ridx].double().cpu().numpy(), res[h][1])
+        check_close("dQ", dq[ridx, h].double().cpu().numpy(), res[h][2])
+    cols = ora.cols_backward(host["q"], host["k"], host["v"], host["do"], cu_h, True, scale,
+                             kv_heads=[1, 2], seg_index=0, col_lo=T - 64)
+    for hk in (1, 2):
+        check_close("dK", dk[T - 64:, hk].double().cpu().numpy(), cols[hk][0])
+        check_close("dV", dv[T - 64:, hk].double().cpu().numpy(), cols[hk][1])
