@@ -118,28 +118,125 @@ def device_pairs(r: int, ranges: Sequence[Sequence[Range]], causal: bool) -> int
     return sum(pair_count(q, k, causal) for q, k, _ in device_steps(r, ranges, causal))
 
 
+def concurrent_groups(calls: Sequence[Tuple[Range, Range, bool]]
+                      ) -> List[List[Tuple[Range, Range, bool]]]:
+    """Split an ordered list of (query range, key range, accumulate) calls
+    into consecutive groups of at most two calls that touch different query
+    ranges and different key ranges: the calls of a group write disjoint
+    dQ and dK/dV rows and may run at the same time, while a call still runs
+    after every earlier call that writes the same rows."""
+    groups: List[List[Tuple[Range, Range, bool]]] = []
+    cur: List[Tuple[Range, Range, bool]] = []
+    for c in calls:
+        if len(cur) < 2 and all(c[0] != o[0] and c[1] != o[1] for o in cur):
+            cur.append(c)
+        else:
+            groups.append(cur)
+            cur = [c]
+    if cur:
+        groups.append(cur)
+    return groups
+
+
+_STREAMS: Dict[object, list] = {}
+
+
+def _side_streams(device) -> list:
+    """Two streams (default priority) for a device's independent calls: a
+    zig-zag device's chunk pairs are separate launches of a few hundred
+    workgroups each, and running two at once fills the tail of each."""
+    import torch
+    key = str(device)
+    if key not in _STREAMS:
+        _STREAMS[key] = [torch.cuda.Stream(device=device) for _ in range(2)]
+    return _STREAMS[key]
+
+
+def forward_chains(steps: Sequence[Tuple[Range, Range, bool]], causal: bool
+                   ) -> List[Tuple[Range, List[Range]]]:
+    """A device's forward calls as independent chains (query range, key
+    ranges in call order): every query range's calls are split in two halves
+    of near-equal work (pairs), each half folded into its own partial result,
+    so that two streams can run them; the first chain of a range starts with
+    its own (diagonal) pair."""
+    by_q: Dict[Range, List[Range]] = {}
+    for q, k, _ in steps:
+        by_q.setdefault(q, []).append(k)
+    chains: List[Tuple[Range, List[Range]]] = []
+    for q, ks in by_q.items():
+        if len(ks) < 2:
+            chains.append((q, ks))
+            continue
+        work = [pair_count(q, k, causal) for k in ks]
+        total, run, cut = sum(work), 0, 1
+        for i, wk in enumerate(work):
+            run += wk
+            if run * 2 >= total:
+                cut = max(1, min(len(ks) - 1, i + 1))
+                break
+        chains.append((q, ks[:cut]))
+        chains.append((q, ks[cut:]))
+    return chains
+
+
 def ring_forward(q, k, v, p: int, causal: bool = True, scale: Optional[float] = None,
                  layout: str = "contiguous", devices: Optional[Iterable[int]] = None,
                  out=None):
     """O [T, Hq, d] and {query range: LSE [Hq, len]} of the sequence, computed
     range pair by range pair in each device's ring order.  `devices` limits
-    the work to those devices' query ranges (the rest of O is left as is)."""
+    the work to those devices' query ranges (the rest of O is left as is).
+    A device's calls run as independent chains on two streams (a chain folds
+    its pairs into its own partial result with attn_merge; the partials of a
+    query range are merged at the end)."""
     import torch
-    ranges = device_ranges(q.shape[0], p, layout)
+    T, hq = q.shape[0], q.shape[1]
+    ranges = device_ranges(T, p, layout)
     o = torch.empty_like(q) if out is None else out
     lses: Dict[Range, object] = {}
+    main = torch.cuda.current_stream(q.device)
+    side = _side_streams(q.device)
     for r in (range(p) if devices is None else devices):
-        acc: Dict[Range, tuple] = {}
-        for (qa, qb), (ka, kb), _ in device_steps(r, ranges, causal):
-            if (qa, qb) not in acc:
-                acc[(qa, qb)] = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka,
-                                                       causal, scale, out=o[qa:qb])
-                continue
-            part = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka, causal, scale)
-            ao, al = acc[(qa, qb)]
-            acc[(qa, qb)] = pdyattn.attn_merge(ao, al, part[0], part[1], out=ao, lse=al)
-        for rg, (_, l) in acc.items():
-            lses[rg] = l
+        chains = forward_chains(device_steps(r, ranges, causal), causal)
+        # outputs and partial results live on the caller's stream
+        parts = []
+        for c, (qr, _) in enumerate(chains):
+            n = qr[1] - qr[0]
+            if qr not in lses:
+                lses[qr] = torch.empty((hq, n), dtype=torch.float32, device=q.device)
+                parts.append((o[qr[0]:qr[1]], lses[qr]))
+            else:
+                parts.append((torch.empty((n,) + tuple(q.shape[1:]), dtype=q.dtype,
+                                          device=q.device),
+                              torch.empty((hq, n), dtype=torch.float32, device=q.device)))
+        # longest chains first, each on the less loaded stream
+        load = [0, 0]
+        order = sorted(range(len(chains)),
+                       key=lambda c: -sum(pair_count(chains[c][0], kr, causal)
+                                          for kr in chains[c][1]))
+        for st in side:
+            st.wait_stream(main)
+        for c in order:
+            (qa, qb), krs = chains[c]
+            si = 0 if load[0] <= load[1] else 1
+            load[si] += sum(pair_count((qa, qb), kr, causal) for kr in krs) + 1
+            po, pl = parts[c]
+            with torch.cuda.stream(side[si]):
+                for j, (ka, kb) in enumerate(krs):
+                    if j == 0:
+                        pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka, causal,
+                                               scale, out=po, lse=pl)
+                    else:
+                        part = pdyattn.attn_fwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], qa, ka,
+                                                      causal, scale)
+                        pdyattn.attn_merge(po, pl, part[0], part[1], out=po, lse=pl)
+        for st in side:
+            main.wait_stream(st)
+        for c, (qr, _) in enumerate(chains):  # fold second halves into the outputs
+            po, pl = parts[c]
+            if po.data_ptr() != o[qr[0]:qr[1]].data_ptr() or qr[0] == qr[1]:
+                if qr[0] < qr[1]:
+                    pdyattn.attn_merge(o[qr[0]:qr[1]], lses[qr], po, pl, out=o[qr[0]:qr[1]],
+                                       lse=lses[qr])
     return o, lses
 
 
@@ -149,7 +246,8 @@ def ring_backward(q, k, v, o, lses: Dict[Range, object], dout, p: int, causal: b
     """dQ [T, Hq, d], dK and dV [T, Hkv, d] (fp32) accumulated in the kernels
     over the range pairs, ring step by ring step.  With `devices` only those
     devices' calls run; a visiting shard's dK/dV then has to arrive in
-    `grads` already holding the earlier devices' sums (zero for a timing)."""
+    `grads` already holding the earlier devices' sums (zero for a timing).
+    Calls that write disjoint rows run two at a time on two streams."""
     import torch
     T, hq, d = q.shape
     hkv = k.shape[1]
@@ -161,16 +259,25 @@ def ring_backward(q, k, v, o, lses: Dict[Range, object], dout, p: int, causal: b
     dq, dk, dv = grads
     devs = list(range(p) if devices is None else devices)
     steps = {r: device_steps(r, ranges, causal) for r in devs}
+    main = torch.cuda.current_stream(q.device)
+    side = _side_streams(q.device)
     # step 0 of every device before any later step: each shard's own device
     # overwrites its dK/dV before other devices add to it
     n_own = {r: sum(1 for _, _, acc in steps[r] if not acc) for r in devs}
     for phase in (0, 1):
         for r in devs:
             calls = steps[r][:n_own[r]] if phase == 0 else steps[r][n_own[r]:]
-            for (qa, qb), (ka, kb), accumulate in calls:
-                pdyattn.attn_bwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], o[qa:qb], lses[(qa, qb)],
-                                       dout[qa:qb], qa, ka, causal, scale, dq=dq[qa:qb],
-                                       dk=dk[ka:kb], dv=dv[ka:kb], accumulate=accumulate)
+            for group in concurrent_groups(calls):
+                for i, ((qa, qb), (ka, kb), accumulate) in enumerate(group):
+                    st = side[i]
+                    st.wait_stream(main)
+                    with torch.cuda.stream(st):
+                        pdyattn.attn_bwd_chunk(q[qa:qb], k[ka:kb], v[ka:kb], o[qa:qb],
+                                               lses[(qa, qb)], dout[qa:qb], qa, ka, causal, scale,
+                                               dq=dq[qa:qb], dk=dk[ka:kb], dv=dv[ka:kb],
+                                               accumulate=accumulate)
+                for i in range(len(group)):
+                    main.wait_stream(side[i])
     return dq, dk, dv
 
 

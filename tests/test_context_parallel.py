@@ -89,3 +89,33 @@ def test_zigzag_balances_causal_work(T, p):
             assert ratio < 1.01
         else:
             assert abs(ratio - (2 * p - 1) / p) < 0.01
+
+
+@pytest.mark.parametrize("layout", ["contiguous", "zigzag"])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("T,p", [(50, 4), (3, 5), (638976, 8)])
+def test_forward_chains_partition_the_calls(layout, causal, T, p):
+    """The forward's chains cover every call of a device exactly once, each
+    chain is non-empty, and a range is split into at most two chains."""
+    ranges = cp.device_ranges(T, p, layout)
+    for r in range(p):
+        steps = cp.device_steps(r, ranges, causal)
+        chains = cp.forward_chains(steps, causal)
+        got = sorted((qr, kr) for qr, krs in chains for kr in krs)
+        assert got == sorted((qr, kr) for qr, kr, _ in steps)
+        assert all(krs for _, krs in chains)
+        per_q = {}
+        for qr, _ in chains:
+            per_q[qr] = per_q.get(qr, 0) + 1
+        assert max(per_q.values()) <= 2
+
+
+def test_concurrent_groups_keep_buffers_apart():
+    calls = [((0, 4), (0, 4), False), ((4, 8), (4, 8), False), ((4, 8), (0, 4), True),
+             ((0, 4), (8, 12), True), ((4, 8), (8, 12), True), ((0, 4), (12, 16), True)]
+    groups = cp.concurrent_groups(calls)
+    assert [c for g in groups for c in g] == calls
+    for g in groups:
+        assert len(g) <= 2
+        if len(g) == 2:
+            assert g[0][0] != g[1][0] and g[0][1] != g[1][1]
