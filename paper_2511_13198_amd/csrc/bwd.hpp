@@ -165,19 +165,29 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int qstart = a.causal ? max(q_lo, k0 - shift) : q_lo;
   const int nqt = max(0, (q_hi - qstart + BQ - 1) / BQ);
   const int nsteps = nqt * g;
+  // a step is one BQ-row tile of one query head of the group: the head's
+  // tiles in row order, then the next head's (tracked incrementally: no
+  // division in the loop)
+  struct StepPos {
+    int h;   // query head
+    int r0;  // first row
+  };
+  const StepPos first = {hk * g, qstart};
+  auto advance = [&](const StepPos& p) __attribute__((always_inline)) {
+    return p.r0 + BQ < q_hi ? StepPos{p.h, p.r0 + BQ} : StepPos{p.h + 1, qstart};
+  };
 
   // threads 0..BQ-1 fetch the LSE of a row, BQ..2BQ-1 its D.  The value is
   // only touched when stored, after the step's products, so the wait for it
   // (which also covers the tile copies issued with it) is not on the
   // critical path.
   float stat = 0.f;
-  auto load_stat = [&](int step) __attribute__((always_inline)) {
+  auto load_stat = [&](const StepPos& p) __attribute__((always_inline)) {
     const int t = threadIdx.x;
     if (t < 2 * BQ) {
-      const int h = hk * g + step / nqt;
-      const int r = qstart + (step % nqt) * BQ + (t % BQ);
+      const int r = p.r0 + (t % BQ);
       const bool ok = r < q_hi;
-      const size_t idx = (size_t)h * a.total_tokens + r;
+      const size_t idx = (size_t)p.h * a.total_tokens + r;
       stat = ok ? (t < BQ ? a.lse[idx] : a.dd[idx]) : 0.f;
     }
   };
@@ -194,13 +204,13 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
 
   // returns false for a wave with nothing to do in this step; `hook(KS)` runs
   // after the products of K-step KS of S/dP (active waves only)
-  auto compute = [&](int step, auto&& hook) __attribute__((always_inline)) {
+  auto compute = [&](int step, const StepPos& p, auto&& hook) __attribute__((always_inline)) {
     const int b = step & 1;
     const uint16_t* qs = qbuf(b);
     const uint16_t* gs = gbuf(b);
     const float* lse_s = stats(b);
     const float* dd_s = lse_s + BQ;
-    const int wr0 = qstart + (step % nqt) * BQ + half * 32;  // first row of this wave
+    const int wr0 = p.r0 + half * 32;  // first row of this wave
     const bool active = (kw0 < k_hi) && (wr0 < q_hi) && (!a.causal || wr0 + 31 + shift >= kw0);
     if (!active) return false;
     const bool need_mask = (a.causal && wr0 + shift < kw0 + 31) || (wr0 + 32 > q_hi);
@@ -293,14 +303,10 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   };
   auto no_hook = [](auto) {};
 
-  auto row_ptr = [&](const uint16_t* t, int step) __attribute__((always_inline)) {
-    const int h = hk * g + step / nqt;
-    const int r0 = qstart + (step % nqt) * BQ;
-    return t + (size_t)r0 * qstride + (size_t)h * D;
+  auto row_ptr = [&](const uint16_t* t, const StepPos& p) __attribute__((always_inline)) {
+    return t + (size_t)p.r0 * qstride + (size_t)p.h * D;
   };
-  auto rows_valid = [&](int step) __attribute__((always_inline)) {
-    return q_hi - (qstart + (step % nqt) * BQ);
-  };
+  auto rows_valid = [&](const StepPos& p) __attribute__((always_inline)) { return q_hi - p.r0; };
 
   // K and V tiles: keys past the segment end read as zeros (d = 128 copies)
   // or repeat the last key (d = 64 loads); their gradients are never written
@@ -317,30 +323,33 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     static_assert(2 * PQ <= D / 16, "one copy per K-step of S/dP");
     QD qd;
     qd.init(qstride);
-    auto issue = [&](int step) __attribute__((always_inline)) {
-      qd.issue(row_ptr(a.q, step), qstride, rows_valid(step), qbuf(step & 1));
-      qd.issue(row_ptr(a.dout, step), qstride, rows_valid(step), gbuf(step & 1));
+    auto issue = [&](int step, const StepPos& p) __attribute__((always_inline)) {
+      qd.issue(row_ptr(a.q, p), qstride, rows_valid(p), qbuf(step & 1));
+      qd.issue(row_ptr(a.dout, p), qstride, rows_valid(p), gbuf(step & 1));
     };
+    StepPos cur = first;
     if (nsteps > 0) {
-      issue(0);
-      load_stat(0);
+      issue(0, cur);
+      load_stat(cur);
     }
     for (int step = 0; step < nsteps; ++step) {
       const bool more = step + 1 < nsteps;
+      // (past the last step `nxt` is only used for address arithmetic)
+      const StepPos nxt = advance(cur);
       // this step's tiles and statistics have landed (they were issued
       // during the previous step); the statistics go to LDS before the barrier
       wait_dma();
       store_stat(step & 1);
       __syncthreads();
-      if (more) load_stat(step + 1);
+      if (more) load_stat(nxt);
       // the next step's copies go out one per K-step of S/dP, so that they
       // trickle into the memory pipeline instead of stalling every wave at once
       // (built for every step; only used when there is a next one)
-      const int rvn = rows_valid(step + 1);
-      const typename QD::Src rsq = QD::src(row_ptr(a.q, step + 1), qstride, rvn);
-      const typename QD::Src rsg = QD::src(row_ptr(a.dout, step + 1), qstride, rvn);
+      const int rvn = rows_valid(nxt);
+      const typename QD::Src rsq = QD::src(row_ptr(a.q, nxt), qstride, rvn);
+      const typename QD::Src rsg = QD::src(row_ptr(a.dout, nxt), qstride, rvn);
       const int bn = (step + 1) & 1;
-      const bool ran = compute(step, [&](auto KS) __attribute__((always_inline)) {
+      const bool ran = compute(step, cur, [&](auto KS) __attribute__((always_inline)) {
         constexpr int c = decltype(KS)::value;
         if constexpr (c < PQ) {
           if (more) qd.issue_one(c, rsq, qbuf(bn));
@@ -348,7 +357,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
           if (more) qd.issue_one(c - PQ, rsg, gbuf(bn));
         }
       });
-      if (!ran && more) issue(step + 1);
+      if (!ran && more) issue(step + 1, nxt);
+      cur = nxt;
     }
   } else {
     {
@@ -359,26 +369,29 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       vl.store(vtile);
     }
     TileLoader<QL, BQ, D, C::NT> ql, gl;
-    auto issue = [&](int step) __attribute__((always_inline)) {
-      ql.load_clamped(row_ptr(a.q, step), qstride, rows_valid(step));
-      gl.load_clamped(row_ptr(a.dout, step), qstride, rows_valid(step));
-      load_stat(step);
+    auto issue = [&](const StepPos& p) __attribute__((always_inline)) {
+      ql.load_clamped(row_ptr(a.q, p), qstride, rows_valid(p));
+      gl.load_clamped(row_ptr(a.dout, p), qstride, rows_valid(p));
+      load_stat(p);
     };
     auto commit = [&](int b) __attribute__((always_inline)) {
       ql.store(qbuf(b));
       gl.store(gbuf(b));
       store_stat(b);
     };
+    StepPos cur = first;
     if (nsteps > 0) {
-      issue(0);
+      issue(cur);
       commit(0);
     }
     for (int step = 0; step < nsteps; ++step) {
       const bool more = step + 1 < nsteps;
-      if (more) issue(step + 1);
+      const StepPos nxt = advance(cur);
+      if (more) issue(nxt);
       __syncthreads();
-      compute(step, no_hook);
+      compute(step, cur, no_hook);
       if (more) commit((step + 1) & 1);
+      cur = nxt;
     }
   }
 
