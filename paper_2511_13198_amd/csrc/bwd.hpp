@@ -511,10 +511,13 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
 
-  auto compute = [&](int it) __attribute__((always_inline)) {
+  // returns false for a wave with nothing to do on this tile; `hook(N)` runs
+  // after the products of the N-th K-step of S^T/dP^T, counted over the
+  // tile's 32-key blocks (active waves only)
+  auto compute = [&](int it, auto&& hook) __attribute__((always_inline)) {
     const int k0 = k_lo + it * BK;
     const bool active = (wrow0 < seg_hi) && (!a.causal || k0 <= wrow_last + shift);
-    if (!active) return;
+    if (!active) return false;
     const uint32_t kra = lds_addr(kbuf(it)) + k_row * 2;
     const uint32_t ka = lds_addr(kbuf(it)) + k_tr * 2;
     const uint32_t vra = lds_addr(vbuf(it)) + v_row * 2;
@@ -543,6 +546,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
           }
           s = mfma32(as_bf16x8(rk[sl]), qf[ks], s);
           dp = mfma32(as_bf16x8(rv[sl]), gf[ks], dp);
+          hook(std::integral_constant<int, kb * NKS + ks>{});
         });
       }
       if (need_mask) {  // diagonal or segment-end tile only
@@ -577,13 +581,21 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
       for (int db = 0; db < NDB; ++db) dqa[db] = mfma32(kt1[db].operand(), sb1, dqa[db]);
       __builtin_amdgcn_s_setprio(0);
     });
+    return true;
   };
 
   // keys past the segment end read as zeros (d = 128 copies) or repeat the
   // last key (d = 64 loads); they are always masked
   if constexpr (D == 128) {
-    TileDma<KL, BK, NW> kd;
-    TileDma<VL, BK, NW> vd;
+    using KD = TileDma<KL, BK, NW>;
+    using VD = TileDma<VL, BK, NW>;
+    // the next tile's copies go out one every GAP K-steps of S^T/dP^T rather
+    // than all at once after the barrier, as in the dK/dV kernel
+    constexpr int PK = KD::PER_WAVE, NCOPY = PK + VD::PER_WAVE;
+    constexpr int GAP = (BK / 32) * (D / 16) / NCOPY;
+    static_assert(GAP >= 1, "one copy per K-step at most");
+    KD kd;
+    VD vd;
     kd.init(kvstride);
     vd.init(kvstride);
     auto issue = [&](int t) __attribute__((always_inline)) {
@@ -594,10 +606,23 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
     // (a chunk can leave a tile without any visible key tile, or with no keys)
     if (ntiles > 0) issue(0);
     for (int it = 0; it < ntiles; ++it) {
+      const bool more = it + 1 < ntiles;
       wait_dma();
       __syncthreads();
-      if (it + 1 < ntiles) issue(it + 1);
-      compute(it);
+      // (built for every tile; only used when there is a next one)
+      const int kt = k_lo + (it + 1) * BK;
+      const typename KD::Src rsk = KD::src(kbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
+      const typename VD::Src rsv = VD::src(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
+      const int bn = (it + 1) & 1;
+      const bool ran = compute(it, [&](auto N) __attribute__((always_inline)) {
+        constexpr int n = decltype(N)::value;
+        if constexpr (n % GAP == 0 && n / GAP < PK) {
+          if (more) kd.issue_one(n / GAP, rsk, kbuf(bn));
+        } else if constexpr (n % GAP == 0 && n / GAP < NCOPY) {
+          if (more) vd.issue_one(n / GAP - PK, rsv, vbuf(bn));
+        }
+      });
+      if (!ran && more) issue(it + 1);
     }
   } else {
     TileLoader<KL, BK, D, C::NT> kl;
@@ -616,7 +641,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
         vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
       }
       __syncthreads();
-      compute(it);
+      compute(it, [](auto) {});
       if (more) {
         kl.store(kbuf(it + 1));
         vl.store(vbuf(it + 1));

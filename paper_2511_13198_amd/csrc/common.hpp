@@ -321,10 +321,14 @@ struct TileDma {
             (int)__builtin_amdgcn_readfirstlane((int)((size_t)rows * gstride * 2))};
   }
   __device__ __forceinline__ static void copy(const Src& s, uint32_t voffset, uint16_t* lds) {
+    // device pass only: in the host pass the buffer-resource type makes a
+    // second kernel's use of the same copy routine fail to instantiate
+#if defined(__HIP_DEVICE_COMPILE__)
     const auto rs = __builtin_amdgcn_make_buffer_rsrc(
         reinterpret_cast<void*>(((uint64_t)s.hi << 32) | s.lo), 0, s.bytes, kBufferFlags);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16,
                                              voffset, 0, 0, 0);
+#endif
   }
   // Copy i of this wave alone (0 <= i < PER_WAVE, a constant at the call
   // site); a no-op where the wave has no copy i.  Lets a kernel spread its
