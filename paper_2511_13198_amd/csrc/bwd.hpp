@@ -5,20 +5,35 @@
 //   dQ = scale * dS K.
 // Three kernels:
 //   * bwd_pre_kernel    D = rowsum(dO * O) (fp32, [Hq, T]) -- bandwidth bound.
-//   * bwd_dkdv_kernel   one workgroup per (segment, kv head, 128-key tile); the
-//                       waves own 32 keys each, keep K and V in registers and
-//                       dK^T / dV^T in accumulators, and sweep every query
-//                       head of the group and every query tile that sees the
-//                       keys.  Written once, no atomics.
-//   * bwd_dq_kernel     one workgroup per (segment, query head, 128-row tile);
-//                       mirrors the forward: recomputes S^T and dP^T, forms
-//                       dS^T and accumulates dQ^T = K^T dS^T.  No atomics.
+//   * bwd_dkdv_kernel   one workgroup per (segment, kv head, 128-key tile); a
+//                       pair of waves owns 32 keys (K and V tiles in LDS),
+//                       keeps dK^T / dV^T in accumulators, and sweeps every
+//                       query head of the group and every 64-row query step
+//                       that sees the keys.  Written once, no atomics.
+//   * bwd_dq_kernel     one workgroup per (segment, query head, 32-row-per-wave
+//                       tile); mirrors the forward: recomputes S^T and dP^T,
+//                       forms dS^T and accumulates dQ^T = K^T dS^T.  No atomics.
+// When a launch cannot fill the chip, a workgroup takes one part of a tile's
+// work (split-K) and split_sum_kernel adds the parts' partial gradients.
 // All outputs are deterministic.
 #pragma once
 #include "common.hpp"
 #include "fwd.hpp"  // acc_row_off
 
 namespace pdy {
+
+// dst = (accumulate ? dst : 0) + sum_p parts[p * n + i] over the nsplit
+// partial gradients of a split-K backward, in part order; 4 floats per
+// thread (n is a multiple of 4: a head dimension of 64 or 128 divides it).
+__global__ void __launch_bounds__(256) split_sum_kernel(const float* __restrict__ parts,
+                                                        int nsplit, size_t n,
+                                                        float* __restrict__ dst, int accumulate) {
+  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  f32x4 acc = accumulate ? *reinterpret_cast<const f32x4*>(dst + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < nsplit; ++p) acc += *reinterpret_cast<const f32x4*>(parts + p * n + i);
+  *reinterpret_cast<f32x4*>(dst + i) = acc;
+}
 
 // D[h][i] = sum_d dO[i,h,d] * O[i,h,d]; one 16-lane group per (row, head).
 template <int D>
@@ -84,6 +99,16 @@ struct BwdArgs {
   int tk;
   int shift;
   int accumulate;  // add to dq/dk/dv instead of overwriting them
+  // split-K (nsplit_* > 1): the work of every dK/dV key tile (its query
+  // steps) or dQ query tile (its key tiles) is cut into contiguous parts, one
+  // workgroup each, and a part writes its scaled partial gradient to
+  // part_dk/part_dv [nsplit_kv][T][Hkv][D] or part_dq [nsplit_q][T][Hq][D]
+  // (fp32, never accumulated) for split_sum_kernel to add up.
+  int nsplit_kv;
+  int nsplit_q;
+  float* part_dk;
+  float* part_dv;
+  float* part_dq;
 };
 
 // dK/dV: one workgroup of 8 waves per (segment, kv head, 128-key tile).  Waves
@@ -117,7 +142,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = C::BK, BQ = C::BQ, NW = C::NW;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
-  const int item = blockIdx.x / a.hkv;
+  // workgroup -> (work item, part of its query steps, kv head)
+  const int item = blockIdx.x / (a.hkv * a.nsplit_kv);
+  const int part = (blockIdx.x / a.hkv) % a.nsplit_kv;
   const int hk = blockIdx.x % a.hkv;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
@@ -164,7 +191,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   // query rows that can see this key tile
   const int qstart = a.causal ? max(q_lo, k0 - shift) : q_lo;
   const int nqt = max(0, (q_hi - qstart + BQ - 1) / BQ);
-  const int nsteps = nqt * g;
+  // this part's steps [s_begin, s_begin + nsteps) of the tile's nqt * g
+  const int s_begin = part * (nqt * g) / a.nsplit_kv;
+  const int nsteps = (part + 1) * (nqt * g) / a.nsplit_kv - s_begin;
   // a step is one BQ-row tile of one query head of the group: the head's
   // tiles in row order, then the next head's (tracked incrementally: no
   // division in the loop)
@@ -172,7 +201,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     int h;   // query head
     int r0;  // first row
   };
-  const StepPos first = {hk * g, qstart};
+  const StepPos first = nqt > 0 ? StepPos{hk * g + s_begin / nqt, qstart + (s_begin % nqt) * BQ}
+                                 : StepPos{hk * g, qstart};
   auto advance = [&](const StepPos& p) __attribute__((always_inline)) {
     return p.r0 + BQ < q_hi ? StepPos{p.h, p.r0 + BQ} : StepPos{p.h + 1, qstart};
   };
@@ -409,8 +439,11 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   }
   __syncthreads();
   if (half == 0 && key < k_hi) {
-    float* dkp = a.dk + (size_t)key * kvstride + (size_t)hk * D;
-    float* dvp = a.dv + (size_t)key * kvstride + (size_t)hk * D;
+    const bool split = a.nsplit_kv > 1;
+    const size_t off = (size_t)key * kvstride + (size_t)hk * D;
+    const size_t poff = (size_t)part * a.total_tokens * kvstride + off;
+    float* dkp = split ? a.part_dk + poff : a.dk + off;
+    float* dvp = split ? a.part_dv + poff : a.dv + off;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -423,7 +456,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
           kv[e] = (dka[db][r] + red[(db * 16 + r) * 64 + l]) * a.scale;
           vv[e] = dva[db][r] + red[32 * D + (db * 16 + r) * 64 + l];
         }
-        if (a.accumulate) {
+        if (a.accumulate && !split) {
           kv += *reinterpret_cast<const f32x4*>(dkp + d0);
           vv += *reinterpret_cast<const f32x4*>(dvp + d0);
         }
@@ -453,7 +486,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   constexpr int BQ = C::BQ, BK = C::BK;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
-  const int item = blockIdx.x / a.hq;
+  // workgroup -> (work item, part of its key tiles, head)
+  const int item = blockIdx.x / (a.hq * a.nsplit_q);
+  const int part = (blockIdx.x / a.hq) % a.nsplit_q;
   const int h = blockIdx.x % a.hq;
   int seg, level;
   if (!plan_lookup(a.plan_q, item, seg, level)) return;
@@ -501,6 +536,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
 
   const int kv_end = a.causal ? min(k_hi, q0 + BQ + shift) : k_hi;
   const int ntiles = max(0, (kv_end - k_lo + BK - 1) / BK);
+  // this part's key tiles [t_begin, t_end) (possibly none)
+  const int t_begin = part * ntiles / a.nsplit_q;
+  const int t_end = (part + 1) * ntiles / a.nsplit_q;
   auto kbuf = [&](int t) __attribute__((always_inline)) { return smem + (t & 1) * C::KTILE; };
   auto vbuf = [&](int t) __attribute__((always_inline)) {
     return smem + 2 * C::KTILE + (t & 1) * C::VTILE;
@@ -604,9 +642,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
       vd.issue(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt, vbuf(t));
     };
     // (a chunk can leave a tile without any visible key tile, or with no keys)
-    if (ntiles > 0) issue(0);
-    for (int it = 0; it < ntiles; ++it) {
-      const bool more = it + 1 < ntiles;
+    if (t_begin < t_end) issue(t_begin);
+    for (int it = t_begin; it < t_end; ++it) {
+      const bool more = it + 1 < t_end;
       wait_dma();
       __syncthreads();
       // (built for every tile; only used when there is a next one)
@@ -627,14 +665,15 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   } else {
     TileLoader<KL, BK, D, C::NT> kl;
     TileLoader<VL, BK, D, C::NT> vl;
-    if (ntiles > 0) {
-      kl.load_clamped(kbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
-      vl.load_clamped(vbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
-      kl.store(kbuf(0));
-      vl.store(vbuf(0));
+    if (t_begin < t_end) {
+      const int k1 = k_lo + t_begin * BK;
+      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
+      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
+      kl.store(kbuf(t_begin));
+      vl.store(vbuf(t_begin));
     }
-    for (int it = 0; it < ntiles; ++it) {
-      const bool more = it + 1 < ntiles;
+    for (int it = t_begin; it < t_end; ++it) {
+      const bool more = it + 1 < t_end;
       if (more) {
         const int k1 = k_lo + (it + 1) * BK;
         kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
@@ -650,7 +689,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   }
 
   if (row < seg_hi) {
-    float* dqp = a.dq + (size_t)row * qstride + (size_t)h * D;
+    const bool split = a.nsplit_q > 1;
+    const size_t off = (size_t)row * qstride + (size_t)h * D;
+    float* dqp = split ? a.part_dq + (size_t)part * a.total_tokens * qstride + off : a.dq + off;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -658,7 +699,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
         const int d0 = db * 32 + grp * 8 + hh * 4;
         f32x4 v = {dqa[db][grp * 4] * a.scale, dqa[db][grp * 4 + 1] * a.scale,
                    dqa[db][grp * 4 + 2] * a.scale, dqa[db][grp * 4 + 3] * a.scale};
-        if (a.accumulate) v += *reinterpret_cast<const f32x4*>(dqp + d0);
+        if (a.accumulate && !split) v += *reinterpret_cast<const f32x4*>(dqp + d0);
         *reinterpret_cast<f32x4*>(dqp + d0) = v;
       }
   }

@@ -73,6 +73,14 @@ struct FwdArgs {
   int chunked;
   int tk;
   int shift;
+  // split-K (nsplit > 1): the key tiles of every query tile are cut into
+  // nsplit contiguous parts, one workgroup each; a part writes its O (fp32,
+  // normalised by its own row sums) to part_o [nsplit][T][Hq][D] and its LSE
+  // to part_lse [nsplit][Hq][T] instead of o / lse, and split_merge_kernel
+  // combines them.  nsplit = 1: o and lse directly.
+  int nsplit;
+  float* part_o;
+  float* part_lse;
 };
 
 // key offset within a 32-key block held in accumulator register r (lane half 0)
@@ -86,7 +94,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   constexpr int BQ = C::BQ, BK = C::BK, BKS = C::BKS;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
-  const int item = blockIdx.x / a.hq;
+  // workgroup -> (work item, part of its keys, head), heaviest items first
+  const int item = blockIdx.x / (a.hq * a.nsplit);
+  const int part = (blockIdx.x / a.hq) % a.nsplit;
   const int h = blockIdx.x % a.hq;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
@@ -130,6 +140,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
 
   const int kv_end = a.causal ? min(k_hi, q0 + BQ + shift) : k_hi;
   const int ntiles = max(0, (kv_end - k_lo + BK - 1) / BK);
+  // this part's key tiles [t_begin, t_end) (possibly none)
+  const int t_begin = part * ntiles / a.nsplit;
+  const int t_end = (part + 1) * ntiles / a.nsplit;
 
   auto kbuf = [&](int t) __attribute__((always_inline)) {
     return smem + (t % C::STAGES) * (C::KTILE + C::VTILE);
@@ -263,14 +276,14 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
     constexpr int kMin = TileDma<KL, BK, NW>::INSTS / NW + TileDma<VL, BK, NW>::INSTS / NW;
 #pragma unroll
     for (int t = 0; t < S - 1; ++t)
-      if (t < ntiles) issue(t);
-    for (int it = 0; it < ntiles; ++it) {
+      if (t_begin + t < t_end) issue(t_begin + t);
+    for (int it = t_begin; it < t_end; ++it) {
       // tiles it+1 .. it+S-2 may still be in flight
-      if (it + S - 2 < ntiles) wait_dma_n<(S - 2) * kMin>();
+      if (it + S - 2 < t_end) wait_dma_n<(S - 2) * kMin>();
       else wait_dma();
       __syncthreads();
       const int tn = it + S - 1;
-      const bool more = tn < ntiles;
+      const bool more = tn < t_end;
       if (active(it)) {
         // the copies of tile tn go out one per K-step of S, so that they
         // trickle into the memory pipeline instead of queueing at once
@@ -313,14 +326,15 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   } else {
     TileLoader<KL, BK, D, C::NT> kl;
     TileLoader<VL, BK, D, C::NT> vl;
-    if (ntiles > 0) {
-      kl.load_clamped(kbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
-      vl.load_clamped(vbase + (size_t)k_lo * kvstride, kvstride, k_hi - k_lo);
-      kl.store(kbuf(0));
-      vl.store(vbuf(0));
+    if (t_begin < t_end) {
+      const int k1 = k_lo + t_begin * BK;
+      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
+      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
+      kl.store(kbuf(t_begin));
+      vl.store(vbuf(t_begin));
     }
-    for (int it = 0; it < ntiles; ++it) {
-      const bool more = it + 1 < ntiles;
+    for (int it = t_begin; it < t_end; ++it) {
+      const bool more = it + 1 < t_end;
       if (more) {
         const int k1 = k_lo + (it + 1) * BK;
         kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
@@ -340,7 +354,23 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
 
   // epilogue: normalise, write O (bf16) and LSE (natural log)
   const float ltot = lsum + partner32(lsum);
-  if (row < seg_hi) {
+  if (row < seg_hi && a.nsplit > 1) {
+    // a part's O in fp32 and its LSE (a part that saw no key: O = 0, LSE = -inf)
+    const bool seen = ltot > 0.f;
+    const float inv = seen ? 1.f / ltot : 0.f;
+    float* op = a.part_o + ((size_t)part * a.total_tokens + row) * qstride + (size_t)h * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 v = {oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv,
+                         oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv};
+        *reinterpret_cast<f32x4*>(op + db * 32 + g * 8 + hh * 4) = v;
+      }
+    if (hh == 0)
+      a.part_lse[((size_t)part * a.hq + h) * a.total_tokens + row] =
+          seen ? (m + __builtin_log2f(ltot)) * kLn2 : -INFINITY;
+  } else if (row < seg_hi) {
     // a row that saw no key (possible for a chunk) gets O = 0, LSE = -inf
     const bool seen = ltot > 0.f;
     const float inv = seen ? 1.f / ltot : 0.f;
@@ -408,6 +438,55 @@ __global__ void __launch_bounds__(256) merge_kernel(const uint16_t* oa, const fl
   }
   *reinterpret_cast<u32x4*>(o + pair * D + sub * 8) = out;
   if (sub == 0) lse[li] = l;
+}
+
+// Combine the nsplit parts of a split-K forward (each over its own key
+// range of the same rows), by the same rule as merge_kernel:
+//   LSE = log sum_p exp(LSE_p),  O = sum_p exp(LSE_p - LSE) O_p,
+// parts with LSE = -inf weigh nothing and a row where every part is -inf
+// gets O = 0, LSE = -inf.  Parts are fp32, O is rounded to bf16 once.  One
+// 8-element slice of a row and head per thread.
+template <int D>
+__global__ void __launch_bounds__(256) split_merge_kernel(const float* part_o,
+                                                          const float* part_lse, int nsplit,
+                                                          uint16_t* o, float* lse,
+                                                          int total_tokens, int hq) {
+  constexpr int LANES = D / 8;
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t pair = gid / LANES;  // row * hq + head
+  const int sub = (int)(gid % LANES);
+  const size_t rows = (size_t)total_tokens * hq;  // (row, head) pairs per part
+  if (pair >= rows) return;
+  const size_t row = pair / hq;
+  const int h = (int)(pair % hq);
+  const size_t li = (size_t)h * total_tokens + row;
+  float mx = -INFINITY;
+  for (int p = 0; p < nsplit; ++p) mx = fmaxf(mx, part_lse[p * rows + li]);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float tot = 0.f;
+  if (mx != -INFINITY) {
+    for (int p = 0; p < nsplit; ++p) {
+      const float w = __expf(part_lse[p * rows + li] - mx);
+      tot += w;
+      const float* src = part_o + (p * rows + pair) * D + sub * 8;
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[i] += w * x0[i];
+        acc[4 + i] += w * x1[i];
+      }
+    }
+  }
+  const float inv = tot > 0.f ? 1.f / tot : 0.f;
+  u32x4 out;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f32x2 x = {acc[2 * i] * inv, acc[2 * i + 1] * inv};
+    out[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
+  }
+  *reinterpret_cast<u32x4*>(o + pair * D + sub * 8) = out;
+  if (sub == 0) lse[li] = tot > 0.f ? mx + __logf(tot) : -INFINITY;
 }
 
 }  // namespace pdy

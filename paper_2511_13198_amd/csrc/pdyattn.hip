@@ -88,9 +88,11 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Optional per-thread kernel timing: while enabled, every launch is bracketed
 // by two events on its own stream; pdy_profile_stop reduces them per kernel.
 // ---------------------------------------------------------------------------
-enum KernelId { K_PLAN = 0, K_FWD, K_PRE, K_DKDV, K_DQ, K_COUNT };
-const char* const kKernelNames[K_COUNT] = {"plan_kernel", "fwd_kernel", "bwd_pre_kernel",
-                                           "bwd_dkdv_kernel", "bwd_dq_kernel"};
+enum KernelId { K_PLAN = 0, K_FWD, K_PRE, K_DKDV, K_DQ, K_SPLIT_MERGE, K_SPLIT_SUM, K_COUNT };
+const char* const kKernelNames[K_COUNT] = {"plan_kernel",        "fwd_kernel",
+                                           "bwd_pre_kernel",     "bwd_dkdv_kernel",
+                                           "bwd_dq_kernel",      "split_merge_kernel",
+                                           "split_sum_kernel"};
 struct ProfRec {
   int kid;
   hipEvent_t a, b;
@@ -136,6 +138,102 @@ size_t plan_bytes(const Sizes& s, int tile) {
 
 size_t dd_bytes(const Sizes& s) { return align256((size_t)s.hq * (size_t)s.T * 4); }
 
+// upper bound on sum_i ceil(len_i / tile) (the number of work items)
+int64_t grid_items(const Sizes& s, int tile) {
+  const int64_t bound1 = s.T / tile + s.N;
+  const int64_t bound2 = s.N * (int64_t)tiles_of(s, tile);
+  return bound1 < bound2 ? bound1 : bound2;
+}
+
+// Split-K.  A launch whose work items cannot fill the chip (fewer than
+// kFillItems workgroups, two per CU) can cut every item's inner loop -- the
+// key tiles of a query tile (forward, dQ) or the query steps of a key tile
+// (dK/dV) -- into 2 or 4 parts, one workgroup each; the parts' fp32 partial
+// results are then combined.  Otherwise the heaviest item alone sets the
+// launch's time (a 16K-token sequence over 4 heads has 256 forward items, the
+// last of which visits every key).  Splitting shortens the heaviest item by
+// (inner - inner/p) tiles but writes and reads back p partial results, so it
+// is taken only while that saves time by the estimate below: a tile's time
+// from the kernels' measured throughput per CU (≈ 4.5 TFLOP/s forward and
+// dK/dV, ≈ 5 dQ), the partial traffic at ≈ 4 TB/s, plus one launch.  The
+// decision depends on the sizes alone, so the workspace queries reproduce
+// it; partial buffers exist only for launches this small (parts x items <
+// 2 kFillItems: at most 1024 x 256 rows of partial results).
+constexpr int64_t kFillItems = 512;
+constexpr int kMaxSplit = 4;
+constexpr double kPartBytesPerUs = 4.0e6;  // partial results written + read back
+constexpr double kLaunchUs = 4.0;          // the combining kernel
+
+// inner: tiles of the heaviest item; tile_us: time of one tile; part_bytes:
+// bytes of one part's partial results
+int split_parts(int64_t items, int64_t inner, double tile_us, double part_bytes) {
+  auto saved = [&](int p) {  // estimated time saved by p parts (p = 1: none)
+    if (p == 1) return 0.0;
+    const int64_t left = (inner + p - 1) / p;
+    return (double)(inner - left) * tile_us - (2.0 * p * part_bytes / kPartBytesPerUs + kLaunchUs);
+  };
+  int p = 1;
+  while (p < kMaxSplit && items * p < kFillItems && inner >= 4 * p && saved(2 * p) > saved(p))
+    p *= 2;
+  return p;
+}
+
+int fwd_key_tile(const Sizes& s) {
+  const bool w8 = fwd_waves(s) == 8;
+  if (s.d == 64) return w8 ? pdy::FwdCfg<64, 8>::BK : pdy::FwdCfg<64, 4>::BK;
+  return w8 ? pdy::FwdCfg<128, 8>::BK : pdy::FwdCfg<128, 4>::BK;
+}
+
+int dq_key_tile(const Sizes& s) {
+  const bool w8 = fwd_waves(s) == 8;
+  if (s.d == 64) return w8 ? pdy::DqCfg<64, 8>::BK : pdy::DqCfg<64, 4>::BK;
+  return w8 ? pdy::DqCfg<128, 8>::BK : pdy::DqCfg<128, 4>::BK;
+}
+
+// microseconds for one CU to process `pairs` (query, key) pairs of one head
+// with `flops_per_pair_d` x d FLOPs each at `tflops` per CU
+double tile_us(double pairs, const Sizes& s, double flops_per_pair_d, double tflops) {
+  return pairs * flops_per_pair_d * (double)s.d / (tflops * 1e6);
+}
+
+int fwd_split(const Sizes& s) {
+  const int rows = 32 * fwd_waves(s), keys = fwd_key_tile(s);
+  return split_parts(grid_items(s, rows) * s.hq, tiles_of(s, keys),
+                     tile_us((double)rows * keys, s, 4.0, 4.5),
+                     (double)s.T * s.hq * s.d * 4);
+}
+
+int dq_split(const Sizes& s) {
+  const int rows = 32 * fwd_waves(s), keys = dq_key_tile(s);
+  return split_parts(grid_items(s, rows) * s.hq, tiles_of(s, keys),
+                     tile_us((double)rows * keys, s, 6.0, 5.0),
+                     (double)s.T * s.hq * s.d * 4);
+}
+
+// the heaviest key tile visits every 64-row query step of every head of its group
+int dkdv_split(const Sizes& s) {
+  const int rows = pdy::DkdvCfg<128>::BQ;
+  return split_parts(grid_items(s, kTile) * s.hkv, (int64_t)tiles_of(s, rows) * (s.hq / s.hkv),
+                     tile_us((double)rows * kTile, s, 8.0, 4.5),
+                     2.0 * s.T * s.hkv * s.d * 4);
+}
+
+size_t part_o_bytes(const Sizes& s, int p) { return align256((size_t)p * s.T * s.hq * s.d * 4); }
+size_t part_lse_bytes(const Sizes& s, int p) { return align256((size_t)p * s.hq * s.T * 4); }
+size_t part_kv_bytes(const Sizes& s, int p) { return align256((size_t)p * s.T * s.hkv * s.d * 4); }
+
+// workspace for a split forward's partial O and LSE (none if it is not split)
+size_t fwd_split_bytes(const Sizes& s) {
+  const int p = fwd_split(s);
+  return p > 1 ? part_o_bytes(s, p) + part_lse_bytes(s, p) : 0;
+}
+
+// workspace for a split backward's partial dK, dV and dQ
+size_t bwd_split_bytes(const Sizes& s) {
+  const int pk = dkdv_split(s), pq = dq_split(s);
+  return (pk > 1 ? 2 * part_kv_bytes(s, pk) : 0) + (pq > 1 ? part_o_bytes(s, pq) : 0);
+}
+
 pdy::Plan make_plan(int32_t* ws, const Sizes& s, int tile) {
   const int nt = tiles_of(s, tile);
   pdy::Plan p;
@@ -144,13 +242,6 @@ pdy::Plan make_plan(int32_t* ws, const Sizes& s, int tile) {
   p.total = ws + 2 * s.N + 2 * nt;
   p.max_nt = nt;
   return p;
-}
-
-// upper bound on sum_i ceil(len_i / tile) (the number of work items)
-int64_t grid_items(const Sizes& s, int tile) {
-  const int64_t bound1 = s.T / tile + s.N;
-  const int64_t bound2 = s.N * (int64_t)tiles_of(s, tile);
-  return bound1 < bound2 ? bound1 : bound2;
 }
 
 template <typename K>
@@ -243,14 +334,15 @@ size_t attn_fwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s, 32 * fwd_waves(s));
+  return plan_bytes(s, 32 * fwd_waves(s)) + fwd_split_bytes(s);
 }
 
 size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s);
+  return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
+         bwd_split_bytes(s);
 }
 
 }  // extern "C"
@@ -273,7 +365,8 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
   pdy_status st;
   const int nw = fwd_waves(s);
   const int tile = 32 * nw;
-  const size_t need = plan_bytes(s, tile);
+  const int nsplit = c.on ? 1 : fwd_split(s);
+  const size_t need = plan_bytes(s, tile) + (nsplit > 1 ? fwd_split_bytes(s) : 0);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -299,7 +392,15 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
   a.chunked = c.on;
   a.tk = c.tk;
   a.shift = c.shift;
-  const dim3 grid((unsigned)(grid_items(s, tile) * s.hq));
+  a.nsplit = nsplit;
+  a.part_o = nullptr;
+  a.part_lse = nullptr;
+  if (nsplit > 1) {
+    uint8_t* w = reinterpret_cast<uint8_t*>(workspace) + plan_bytes(s, tile);
+    a.part_o = reinterpret_cast<float*>(w);
+    a.part_lse = reinterpret_cast<float*>(w + part_o_bytes(s, nsplit));
+  }
+  const dim3 grid((unsigned)(grid_items(s, tile) * s.hq * nsplit));
   e = launch_timed(K_FWD, hs, [&] {
     if (s.d == 64) {
       if (nw == 8) launch_fwd<64, 8>(grid, hs, a);
@@ -310,6 +411,20 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
     }
   });
   if (e != hipSuccess) return hip_fail(e, "fwd_kernel launch");
+  if (nsplit > 1) {
+    const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
+    const dim3 blocks((unsigned)((threads + 255) / 256));
+    e = launch_timed(K_SPLIT_MERGE, hs, [&] {
+      uint16_t* out = static_cast<uint16_t*>(o);
+      if (s.d == 64)
+        hipLaunchKernelGGL(pdy::split_merge_kernel<64>, blocks, dim3(256), 0, hs, a.part_o,
+                           a.part_lse, nsplit, out, lse, (int)s.T, (int)s.hq);
+      else
+        hipLaunchKernelGGL(pdy::split_merge_kernel<128>, blocks, dim3(256), 0, hs, a.part_o,
+                           a.part_lse, nsplit, out, lse, (int)s.T, (int)s.hq);
+    });
+    if (e != hipSuccess) return hip_fail(e, "split_merge_kernel launch");
+  }
   return PDY_OK;
 }
 
@@ -326,7 +441,10 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   pdy_status st;
   const int nwq = fwd_waves(s);
   const int qtile = 32 * nwq;
-  const size_t need = bwd_need(s, sk);
+  // split-K only for self-attention over cu's segments (sk is then s)
+  const int nsplit_kv = c.on ? 1 : dkdv_split(s);
+  const int nsplit_q = c.on ? 1 : dq_split(s);
+  const size_t need = bwd_need(s, sk) + (c.on ? 0 : bwd_split_bytes(s));
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -379,8 +497,28 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   a.tk = c.tk;
   a.shift = c.shift;
   a.accumulate = c.accumulate;
+  a.nsplit_kv = nsplit_kv;
+  a.nsplit_q = nsplit_q;
+  a.part_dk = a.part_dv = a.part_dq = nullptr;
+  {
+    uint8_t* w = reinterpret_cast<uint8_t*>(workspace) + bwd_need(s, sk);
+    if (nsplit_kv > 1) {
+      a.part_dk = reinterpret_cast<float*>(w);
+      a.part_dv = reinterpret_cast<float*>(w + part_kv_bytes(s, nsplit_kv));
+      w += 2 * part_kv_bytes(s, nsplit_kv);
+    }
+    if (nsplit_q > 1) a.part_dq = reinterpret_cast<float*>(w);
+  }
+  // the parts' partial gradients, summed into dst
+  auto sum_parts = [&](const float* parts, int nsplit, size_t n, float* dst) {
+    const dim3 blocks((unsigned)((n / 4 + 255) / 256));
+    return launch_timed(K_SPLIT_SUM, hs, [&] {
+      hipLaunchKernelGGL(pdy::split_sum_kernel, blocks, dim3(256), 0, hs, parts, nsplit, n, dst,
+                         c.accumulate);
+    });
+  };
   if (sk.T > 0) {
-    const dim3 gkv((unsigned)(grid_items(sk, kTile) * s.hkv));
+    const dim3 gkv((unsigned)(grid_items(sk, kTile) * s.hkv * nsplit_kv));
     e = launch_timed(K_DKDV, hs, [&] {
       if (s.d == 64)
         hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
@@ -390,8 +528,14 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
                            pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
     });
     if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
+    if (nsplit_kv > 1) {
+      const size_t n = (size_t)sk.T * s.hkv * s.d;
+      if ((e = sum_parts(a.part_dk, nsplit_kv, n, dk)) != hipSuccess ||
+          (e = sum_parts(a.part_dv, nsplit_kv, n, dv)) != hipSuccess)
+        return hip_fail(e, "split_sum_kernel launch");
+    }
   }
-  const dim3 gq((unsigned)(grid_items(s, qtile) * s.hq));
+  const dim3 gq((unsigned)(grid_items(s, qtile) * s.hq * nsplit_q));
   e = launch_timed(K_DQ, hs, [&] {
     if (s.d == 64) {
       if (nwq == 8) launch_dq<64, 8>(gq, hs, a);
@@ -402,6 +546,9 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     }
   });
   if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
+  if (nsplit_q > 1 &&
+      (e = sum_parts(a.part_dq, nsplit_q, (size_t)s.T * s.hq * s.d, dq)) != hipSuccess)
+    return hip_fail(e, "split_sum_kernel launch");
   return PDY_OK;
 }
 

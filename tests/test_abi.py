@@ -101,12 +101,35 @@ def test_workspace_sizes():
     assert P.bwd_workspace_size(512, 1, 513, 8, 8, 128) == 0
 
 
+MiB = 1 << 20
+
+
+def test_split_k_workspace():
+    """Launches too small to fill the chip split their work (split-K) and need
+    fp32 partial buffers; the size queries make the same decision as the
+    calls.  8192 tokens x 4 heads: forward and dQ in 4 parts, dK/dV in 2."""
+    part_o = 4 * 8192 * 4 * 128 * 4
+    assert P.fwd_workspace_size(8192, 1, 8192, 4, 4, 128) >= part_o + 4 * 4 * 8192 * 4
+    assert P.bwd_workspace_size(8192, 1, 8192, 4, 4, 128) >= 2 * (2 * 8192 * 4 * 128 * 4) + part_o
+    # grouped heads at 16K: only dK/dV (2 kv heads) splits, in 2 parts
+    b = P.bwd_workspace_size(16384, 1, 16384, 8, 2, 128)
+    assert 2 * (2 * 16384 * 2 * 128 * 4) <= b < 2 * (2 * 16384 * 2 * 128 * 4) + 2 * MiB
+    # launches that fill the chip need no partial buffers
+    assert P.fwd_workspace_size(131072, 1, 131072, 4, 4, 128) < MiB
+    assert P.bwd_workspace_size(16384, 1, 16384, 8, 8, 64) < 2 * MiB
+    # segments of at most 128 tokens leave nothing to split
+    assert P.fwd_workspace_size(1024, 8, 128, 1, 1, 64) < MiB
+    # chunk calls never split
+    assert P.fwd_chunk_workspace_size(8192, 8192, 4, 4, 128) < MiB
+
+
 def test_status_strings_and_kernel_names():
     L = P.lib()
     assert L.pdy_status_string(0) == b"ok"
     assert L.pdy_status_string(-3) == b"workspace too small"
     names = [L.pdy_kernel_name(i).decode() for i in range(L.pdy_kernel_count())]
-    assert {"fwd_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel"} <= set(names)
+    assert {"fwd_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel", "split_merge_kernel",
+            "split_sum_kernel"} <= set(names)
     # profiling with nothing launched reports nothing
     P.profile_start()
     assert P.profile_stop() == {}
