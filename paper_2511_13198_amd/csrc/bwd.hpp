@@ -116,7 +116,9 @@ struct BwdArgs {
 // shared by the workgroup) and split every 64-row query step: wave w takes rows
 // 0..31, wave w+4 rows 32..63.  Two waves per SIMD let one wave's softmax
 // recomputation overlap the other's matrix products.  The pair's dK^T/dV^T
-// accumulators are summed through LDS once at the end.
+// accumulators are summed through LDS once at the end.  Under split-K a
+// workgroup takes one contiguous part of the tile's query steps and writes
+// partial dK/dV for split_sum_kernel.
 template <int D>
 struct DkdvCfg {
   static constexpr int BK = 128;  // keys per workgroup (32 per wave pair)

@@ -10,10 +10,14 @@
 // tile; the row max / row sum need one cross-half exchange (permlane32_swap).
 // The probabilities are rounded to bf16 and fed back as the B operand of
 //   O^T += V^T P^T          (32 head-dim x 32 rows per MFMA tile)
-// with V^T read from the row-major LDS tile by transposing reads.  K/V tiles of
-// 64 keys are staged through LDS: the global loads of tile t+1 are in flight
-// while tile t is computed.  Tiles entirely above the causal diagonal are never
-// visited; only tiles crossing the diagonal or the segment end are masked.
+// with V^T read from the row-major LDS tile by transposing reads.  K/V tiles
+// (128 keys at d = 128 with 8 waves, else 64) reach LDS by direct copies
+// (d = 128) or through registers (d = 64); tile t+1 is in flight while tile t
+// is computed, in softmax steps of 64 keys.  Tiles entirely above the causal
+// diagonal are never visited; only tiles crossing the diagonal or the segment
+// end are masked.  When a launch has too few query tiles to fill the chip, a
+// workgroup takes one contiguous part of its query tile's key tiles (split-K)
+// and writes a partial O and LSE that split_merge_kernel combines.
 //
 // Softmax statistics are kept in base 2 (log2(e) folded into the scale).  The
 // running max used as the exponent offset is only raised when a new tile's max
