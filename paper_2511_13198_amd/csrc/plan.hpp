@@ -8,17 +8,62 @@
 // which balances the tail of a launch when lengths are skewed.  The list is
 // never materialised: the plan stores the segments sorted by tile count and
 // the first item index of every level, and a kernel maps its item index to
-// (segment, level) with a binary search (plan_lookup in common.hpp).
+// (segment, level) with a binary search (plan_lookup in common.hpp).  The
+// plan costs O(N + max_nt) per launch, also for batches of very many short
+// segments.
 #pragma once
 #include "common.hpp"
 
 namespace pdy {
 
 constexpr int kPlanThreads = 1024;
+// tile counts up to this many are binned in LDS (786,432 tokens at 128-token
+// tiles); larger ranges bin in the workspace
+constexpr int kLdsBuckets = 6144;
 
 // Workspace layout (int32): nt[N] | order[N] | cnt[max_nt] | start[max_nt] | total[1]
 __host__ __device__ inline size_t plan_ints(int n, int max_nt) {
   return (size_t)2 * n + (size_t)2 * max_nt + 1;
+}
+
+// In-place suffix sum over a[0..n) by the whole workgroup: a[j] becomes
+// sum_{j' >= j} a[j'] (inclusive) or sum_{j' > j} a[j'] (exclusive).  Each
+// thread owns a chunk of consecutive entries counted from the top; thread 0
+// scans the per-thread totals in `part`.  Returns the sum of all entries.
+__device__ inline int suffix_sum(int32_t* a, int n, bool inclusive, int32_t* part) {
+  const int t = threadIdx.x;
+  const int chunk = (n + kPlanThreads - 1) / kPlanThreads;
+  int local = 0;
+  for (int c = 0; c < chunk; ++c) {
+    const int idx = t * chunk + c;
+    if (idx < n) local += a[n - 1 - idx];
+  }
+  part[t] = local;
+  __syncthreads();
+  if (t == 0) {
+    int run = 0;
+    for (int i = 0; i < kPlanThreads; ++i) {
+      const int v = part[i];
+      part[i] = run;
+      run += v;
+    }
+    part[kPlanThreads] = run;
+  }
+  __syncthreads();
+  int run = part[t];
+  for (int c = 0; c < chunk; ++c) {
+    const int idx = t * chunk + c;
+    if (idx < n) {
+      const int j = n - 1 - idx;
+      const int v = a[j];
+      if (inclusive) run += v;
+      a[j] = run;
+      if (!inclusive) run += v;
+    }
+  }
+  const int total = part[kPlanThreads];
+  __syncthreads();
+  return total;
 }
 
 // cu == nullptr: a single segment of single_len tokens (n must be 1)
@@ -31,67 +76,53 @@ plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int singl
   int32_t* start = cnt + max_nt;
   int32_t* total = start + max_nt;
   const int t = threadIdx.x;
-  __shared__ int32_t part[kPlanThreads];
+  __shared__ int32_t part[kPlanThreads + 1];
+  // per-count histogram and placement cursors: in LDS when they fit (many
+  // segments with the same count then contend in LDS, not in L2)
+  __shared__ int32_t lds_hist[kLdsBuckets];
+  __shared__ int32_t lds_cur[kLdsBuckets];
+  const bool in_lds = max_nt <= kLdsBuckets;
+  int32_t* hist = in_lds ? lds_hist : cnt;
+  int32_t* cur = in_lds ? lds_cur : start;
 
-  // 1. tiles per segment
+  // 1. tiles per segment, and hist[v - 1] = number of segments with v tiles
+  for (int j = t; j < max_nt; j += kPlanThreads) {
+    hist[j] = 0;
+    cur[j] = 0;
+  }
+  __syncthreads();
   for (int s = t; s < n; s += kPlanThreads) {
     const int len = cu ? cu[s + 1] - cu[s] : single_len;
     int v = (len + bt - 1) / bt;
-    nt[s] = v < max_nt ? v : max_nt;  // max_seqlen is a caller-guaranteed bound
+    v = v < max_nt ? v : max_nt;  // max_seqlen is a caller-guaranteed bound
+    nt[s] = v;
+    if (v > 0) atomicAdd(&hist[v - 1], 1);
   }
-  for (int j = t; j < max_nt; j += kPlanThreads) cnt[j] = 0;
   __syncthreads();
 
-  // 2. rank by (tile count desc, index asc); the rank is a permutation
+  // 2. cnt[j] = number of segments with more than j tiles
+  if (in_lds) {
+    for (int j = t; j < max_nt; j += kPlanThreads) cnt[j] = hist[j];
+    __syncthreads();
+  }
+  suffix_sum(cnt, max_nt, true, part);
+
+  // 3. order: segments by tile count, most first (a counting sort: the ones
+  // with v tiles fill positions [cnt[v], cnt[v - 1]) through the per-count
+  // cursor).  The order among segments with the same count depends on the
+  // atomics' timing, which changes which workgroup runs an item but not what
+  // the item computes.
   for (int s = t; s < n; s += kPlanThreads) {
-    const int mine = nt[s];
-    int rank = 0;
-    for (int o = 0; o < n; ++o) {
-      const int other = nt[o];
-      rank += (other > mine) || (other == mine && o < s);
-    }
-    order[rank] = s;
+    const int v = nt[s];
+    if (v > 0) order[(v < max_nt ? cnt[v] : 0) + atomicAdd(&cur[v - 1], 1)] = s;
   }
   __syncthreads();
 
-  // 3. cnt[j] = number of segments with more than j tiles
-  for (int r = t; r < n; r += kPlanThreads) {
-    const int hi = nt[order[r]];
-    const int lo = (r + 1 < n) ? nt[order[r + 1]] : 0;
-    for (int j = lo; j < hi; ++j) cnt[j] = r + 1;
-  }
+  // 4. start[j] = sum_{j' > j} cnt[j'] (first item of level j); total items
+  for (int j = t; j < max_nt; j += kPlanThreads) start[j] = cnt[j];
   __syncthreads();
-
-  // 4. start[j] = sum_{j' > j} cnt[j'] (exclusive suffix sum), chunked scan
-  const int chunk = (max_nt + kPlanThreads - 1) / kPlanThreads;
-  // thread t owns levels counted from the top: idx = t*chunk .. t*chunk+chunk-1,
-  // level = max_nt - 1 - idx
-  int local = 0;
-  for (int c = 0; c < chunk; ++c) {
-    const int idx = t * chunk + c;
-    if (idx < max_nt) local += cnt[max_nt - 1 - idx];
-  }
-  part[t] = local;
-  __syncthreads();
-  if (t == 0) {
-    int run = 0;
-    for (int i = 0; i < kPlanThreads; ++i) {
-      const int v = part[i];
-      part[i] = run;
-      run += v;
-    }
-    *total = run;
-  }
-  __syncthreads();
-  int run = part[t];
-  for (int c = 0; c < chunk; ++c) {
-    const int idx = t * chunk + c;
-    if (idx < max_nt) {
-      const int j = max_nt - 1 - idx;
-      start[j] = run;
-      run += cnt[j];
-    }
-  }
+  const int items = suffix_sum(start, max_nt, false, part);
+  if (t == 0) *total = items;
 }
 
 }  // namespace pdy

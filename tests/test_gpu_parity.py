@@ -126,9 +126,13 @@ def test_determinism_and_isolation(lengths, hq, hkv):
 # Full-size workloads: sampled parity + invariants
 # ---------------------------------------------------------------------------
 def _sampled_parity(w: wl.Workload, device_gen: bool, heads, kv_heads, per_seg_random,
-                    tail_cols, tail_segs=None, max_rows=None, expect_split=None):
+                    tail_cols, tail_segs=None, max_rows=None, expect_split=None,
+                    invariants=True, max_plan_ms=None, max_seqlen=None):
     """expect_split: {"merge": n, "sum": m} -- the split-K combining kernels the
-    forward + backward must launch (checked with the library's launch counters)."""
+    forward + backward must launch; max_plan_ms: bound on the tile schedule's
+    time per launch (both checked with the library's launch counters).
+    invariants: the whole-tensor gradient identities (one pass per segment).
+    max_seqlen: the bound passed to the library (default: the true maximum)."""
     import torch
     from paper_2511_13198_amd import pdyattn
     T, hq, hkv, d = w.total_tokens, w.heads_q, w.heads_kv, w.head_dim
@@ -141,18 +145,25 @@ def _sampled_parity(w: wl.Workload, device_gen: bool, heads, kv_heads, per_seg_r
         dev = {n: pu.to_device_bf16(b) for n, b in bits.items()}
     cu = w.cu_seqlens()
     cu_d = torch.from_numpy(cu).cuda()
-    if expect_split is not None:
+    counted = expect_split is not None or max_plan_ms is not None
+    if counted:
         pdyattn.profile_start()
     o, lse, dq, dk, dv = pu.run_gpu(dev["q"], dev["k"], dev["v"], dev["do"], cu_d,
-                                    w.max_seqlen, w.causal, scale)
-    if expect_split is not None:
+                                    max_seqlen or w.max_seqlen, w.causal, scale)
+    if counted:
         prof = pdyattn.profile_stop()
+    if expect_split is not None:
         got = {"merge": prof.get("split_merge_kernel", (0, 0.0))[0],
                "sum": prof.get("split_sum_kernel", (0, 0.0))[0]}
         assert got == expect_split, f"split-K launches {got}, expected {expect_split}"
+    if max_plan_ms is not None:
+        launches, total_ms = prof["plan_kernel"]
+        pu.log(f"  plan_kernel {total_ms / launches:.4f} ms per launch")
+        assert total_ms / launches < max_plan_ms, f"plan {total_ms / launches:.3f} ms per launch"
     cu_list = [int(x) for x in cu]
-    pu.gpu_invariants(o, lse, dq, dk, dv, dev["q"], dev["k"], dev["v"], dev["do"], cu_list,
-                      scale, w.causal)
+    if invariants:
+        pu.gpu_invariants(o, lse, dq, dk, dv, dev["q"], dev["k"], dev["v"], dev["do"], cu_list,
+                          scale, w.causal)
     host = {n: pu.HeadView(t) for n, t in dev.items()}
     rows = pu.sample_rows(w.lengths, per_seg_random, max_rows=max_rows)
     res = ora.rows_forward_backward(host["q"], host["k"], host["v"], host["do"], cu, w.causal,
@@ -206,6 +217,35 @@ def test_split_k(lengths, hq, hkv, d, expect):
     _sampled_parity(w, device_gen=False, heads=[0, hq - 1], kv_heads=[0, hkv - 1],
                     per_seg_random=24, tail_cols=192, tail_segs=list(range(len(lengths))),
                     expect_split=expect)
+
+
+@pytest.mark.parametrize("nseg,hi,hq,hkv,d", [
+    (16384, 64, 2, 1, 64),    # every segment <= 128 tokens: the 4-wave kernels
+    (6000, 300, 4, 2, 128),   # 8-wave kernels
+])
+def test_many_segments(nseg, hi, hq, hkv, d):
+    """Batches of thousands of short segments (lengths uniform in 1..hi): the
+    tile schedule is a counting sort, far below a millisecond per launch, and
+    sampled rows and the tail key columns of three segments match the oracle."""
+    rng = np.random.default_rng(7)
+    lengths = [int(x) for x in rng.integers(1, hi + 1, size=nseg)]
+    w = wl.Workload(f"many{nseg}x{hi}", lengths, hq, hkv, d)
+    _sampled_parity(w, device_gen=True, heads=[0, hq - 1], kv_heads=[0, hkv - 1],
+                    per_seg_random=0, tail_cols=hi, tail_segs=[0, nseg // 2, nseg - 1],
+                    max_rows=512, invariants=False, max_plan_ms=0.5)
+
+
+def test_plan_with_a_loose_length_bound():
+    """max_seqlen only bounds the segment lengths: 1000 segments (about 800K
+    tokens, one head) passed with max_seqlen = T give more tile counts than
+    the schedule bins in LDS, so it bins in the workspace instead."""
+    rng = np.random.default_rng(11)
+    lengths = [int(x) for x in rng.integers(1, 1601, size=1000)]
+    w = wl.Workload("loose_bound", lengths, 1, 1, 64)
+    assert w.total_tokens // 128 > 6144
+    _sampled_parity(w, device_gen=True, heads=[0], kv_heads=[0], per_seg_random=0,
+                    tail_cols=128, tail_segs=[0, 500, 999], max_rows=384, invariants=False,
+                    max_plan_ms=0.5, max_seqlen=w.total_tokens)
 
 
 def test_single_638976_h4():
