@@ -144,10 +144,16 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BK = C::BK, BQ = C::BQ, NW = C::NW;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
-  // workgroup -> (work item, part of its query steps, kv head)
-  const int item = blockIdx.x / (a.hkv * a.nsplit_kv);
-  const int part = (blockIdx.x / a.hkv) % a.nsplit_kv;
-  const int hk = blockIdx.x % a.hkv;
+  // workgroup -> (kv head, work item, part of its query steps).  A
+  // workgroup streams the query rows from its key tile on; the XCD-aware
+  // order keeps those of the workgroups running at a time on one XCD within
+  // its L2 (with 2 kv heads and plain round-robin, each XCD would stream
+  // every fourth key tile's rows: an 8 MB window and 20x the traffic beyond
+  // L2)
+  int hk, entry;
+  xcd_order(blockIdx.x, gridDim.x, a.hkv, hk, entry);
+  const int item = entry / a.nsplit_kv;
+  const int part = entry % a.nsplit_kv;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
   // keys [k_lo, k_hi) (this workgroup: a tile of them), query rows

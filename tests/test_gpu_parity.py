@@ -235,6 +235,14 @@ def test_many_segments(nseg, hi, hq, hkv, d):
                     max_rows=512, invariants=False, max_plan_ms=0.5)
 
 
+def test_single_65536_one_kv_head():
+    """4 query heads on one kv head (one GPU's share of a 32/8-head model over
+    8 GPUs): the dK/dV workgroups run in the XCD order for few kv heads."""
+    w = wl.Workload("single65536_h4kv1", [65536], 4, 1, 128)
+    _sampled_parity(w, device_gen=True, heads=[0, 3], kv_heads=[0], per_seg_random=48,
+                    tail_cols=256, expect_split={"merge": 0, "sum": 0})
+
+
 def test_plan_with_a_loose_length_bound():
     """max_seqlen only bounds the segment lengths: 1000 segments (about 800K
     tokens, one head) passed with max_seqlen = T give more tile counts than
