@@ -203,16 +203,21 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int s_begin = part * (nqt * g) / a.nsplit_kv;
   const int nsteps = (part + 1) * (nqt * g) / a.nsplit_kv - s_begin;
   // a step is one BQ-row tile of one query head of the group: the head's
-  // tiles in row order, then the next head's (tracked incrementally: no
-  // division in the loop)
+  // tiles from the last row down to the key tile (the causal diagonal comes
+  // last), then the next head's; tracked incrementally (no division in the
+  // loop).  Top-down, the workgroups an XCD runs at a time, which hold
+  // neighbouring key tiles, start on the same rows and stay close, so the
+  // rows they stream are shared in L2 (bottom-up they are a few steps apart
+  // and drift further with every head: measured 0.8-1.1 % slower)
   struct StepPos {
     int h;   // query head
     int r0;  // first row
   };
-  const StepPos first = nqt > 0 ? StepPos{hk * g + s_begin / nqt, qstart + (s_begin % nqt) * BQ}
+  const int r_last = qstart + (nqt - 1) * BQ;
+  const StepPos first = nqt > 0 ? StepPos{hk * g + s_begin / nqt, r_last - (s_begin % nqt) * BQ}
                                  : StepPos{hk * g, qstart};
   auto advance = [&](const StepPos& p) __attribute__((always_inline)) {
-    return p.r0 + BQ < q_hi ? StepPos{p.h, p.r0 + BQ} : StepPos{p.h + 1, qstart};
+    return p.r0 > qstart ? StepPos{p.h, p.r0 - BQ} : StepPos{p.h + 1, r_last};
   };
 
   // threads 0..BQ-1 fetch the LSE of a row, BQ..2BQ-1 its D.  The value is
