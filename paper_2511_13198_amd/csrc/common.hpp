@@ -378,20 +378,21 @@ struct Plan {
 // n = nheads x (entries per head).  The hardware deals workgroups to the 8
 // XCDs round-robin (workgroup b runs on XCD b % 8; each XCD has 32 CUs and
 // its own L2), so with head = b % nheads and entry = b / nheads a head is
-// spread over 8 / nheads XCDs, each taking every (8 / nheads)-th entry.  For
-// one or two heads that spreads what the entries running at a time stream
-// over a window too wide for an L2, so there each of the head's XCDs instead
-// takes 32 consecutive entries of the head's heaviest-first list at a time
-// (the blocks of a head's XCDs run in reverse order every other round, so no
-// XCD always gets the lightest block).  Measured on the dK/dV kernel at
-// 131,072 tokens: 1 kv head -4.7 %, 2 kv heads -3.9 %, 4 heads no gain (the
-// plain order is kept there).  A bijection on [0, n); the last partial round
-// keeps the plain order.
+// spread over 8 / nheads XCDs, each taking every (8 / nheads)-th entry, and
+// what the entries running at a time on one XCD stream spreads over a wide
+// window.  When nheads divides 8, each of a head's XCDs instead takes 32
+// consecutive entries of the head's heaviest-first list at a time (the
+// blocks of a head's XCDs run in reverse order every other round, so no XCD
+// always gets the lightest block; with 8 heads this is the plain order).
+// Measured on the dK/dV kernel at 131,072 tokens: 1 kv head -4.7 %, 2 kv
+// heads -3.9 %, 4 kv heads -0.3 to -0.8 %.  Other head counts keep the
+// plain order.  A bijection on [0, n); the last partial round keeps the
+// plain order.
 __device__ __forceinline__ void xcd_order(int b, int n, int nheads, int& head, int& entry) {
   constexpr int kXcd = 8, kPer = 32, kRound = kXcd * kPer;
   head = b % nheads;
   entry = b / nheads;
-  if (nheads > 2 || b >= n / kRound * kRound) return;
+  if (kXcd % nheads != 0 || b >= n / kRound * kRound) return;
   const int g = kXcd / nheads;          // XCDs per head
   const int sub = (b % kXcd) / nheads;  // which of them
   const int s = b / kXcd;               // workgroup index on this XCD
