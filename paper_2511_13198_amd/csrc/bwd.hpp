@@ -499,10 +499,12 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   constexpr int BQ = C::BQ, BK = C::BK;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
-  // workgroup -> (work item, part of its key tiles, head)
-  const int item = blockIdx.x / (a.hq * a.nsplit_q);
-  const int part = (blockIdx.x / a.hq) % a.nsplit_q;
-  const int h = blockIdx.x % a.hq;
+  // workgroup -> (head, work item, part of its key tiles), in the XCD-aware
+  // order, as in the forward
+  int h, entry;
+  xcd_order(blockIdx.x, gridDim.x, a.hq, h, entry);
+  const int item = entry / a.nsplit_q;
+  const int part = entry % a.nsplit_q;
   int seg, level;
   if (!plan_lookup(a.plan_q, item, seg, level)) return;
   // query rows [seg_lo, seg_hi), keys [k_lo, k_hi); causal: key j visible to

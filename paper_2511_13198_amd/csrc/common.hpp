@@ -384,9 +384,9 @@ struct Plan {
 // consecutive entries of the head's heaviest-first list at a time (the
 // blocks of a head's XCDs run in reverse order every other round, so no XCD
 // always gets the lightest block; with 8 heads this is the plain order).
-// Measured on the dK/dV kernel at 131,072 tokens: 1 kv head -4.7 %, 2 kv
-// heads -3.9 %, 4 kv heads -0.3 to -0.8 %.  Other head counts keep the
-// plain order.  A bijection on [0, n); the last partial round keeps the
+// Measured at 131,072 tokens: dK/dV with 1 kv head -4.7 %, 2 kv heads
+// -3.9 %, 4 kv heads -0.3 to -0.8 %; forward and dQ with 4 query heads
+// -1.4 % and -0.6 %.  Other head counts keep the plain order.  A bijection on [0, n); the last partial round keeps the
 // plain order.
 __device__ __forceinline__ void xcd_order(int b, int n, int nheads, int& head, int& entry) {
   constexpr int kXcd = 8, kPer = 32, kRound = kXcd * kPer;

@@ -98,10 +98,14 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   constexpr int BQ = C::BQ, BK = C::BK, BKS = C::BKS;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
-  // workgroup -> (work item, part of its keys, head), heaviest items first
-  const int item = blockIdx.x / (a.hq * a.nsplit);
-  const int part = (blockIdx.x / a.hq) % a.nsplit;
-  const int h = blockIdx.x % a.hq;
+  // workgroup -> (head, work item, part of its keys), heaviest items first,
+  // in the XCD-aware order: the workgroups an XCD runs at a time hold
+  // neighbouring query tiles of one head, which stream the same K/V tiles
+  // from key 0 and finish close together (4 heads: 1.4 % faster)
+  int h, entry;
+  xcd_order(blockIdx.x, gridDim.x, a.hq, h, entry);
+  const int item = entry / a.nsplit;
+  const int part = entry % a.nsplit;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
   // query rows [seg_lo, seg_hi), keys [k_lo, k_hi); causal: key j visible to
