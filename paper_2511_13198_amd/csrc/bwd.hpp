@@ -102,8 +102,9 @@ struct BwdArgs {
   // split-K (nsplit_* > 1): the work of every dK/dV key tile (its query
   // steps) or dQ query tile (its key tiles) is cut into contiguous parts, one
   // workgroup each, and a part writes its scaled partial gradient to
-  // part_dk/part_dv [nsplit_kv][T][Hkv][D] or part_dq [nsplit_q][T][Hq][D]
-  // (fp32, never accumulated) for split_sum_kernel to add up.
+  // part_dk/part_dv [nsplit_kv][keys][Hkv][D] or part_dq [nsplit_q][T][Hq][D]
+  // (fp32, never accumulated; keys = tk for a chunk, else T) for
+  // split_sum_kernel to add up.
   int nsplit_kv;
   int nsplit_q;
   float* part_dk;
@@ -454,7 +455,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   if (half == 0 && key < k_hi) {
     const bool split = a.nsplit_kv > 1;
     const size_t off = (size_t)key * kvstride + (size_t)hk * D;
-    const size_t poff = (size_t)part * a.total_tokens * kvstride + off;
+    const size_t poff = (size_t)part * (a.chunked ? a.tk : a.total_tokens) * kvstride + off;
     float* dkp = split ? a.part_dk + poff : a.dk + off;
     float* dvp = split ? a.part_dv + poff : a.dv + off;
 #pragma unroll

@@ -196,26 +196,29 @@ double tile_us(double pairs, const Sizes& s, double flops_per_pair_d, double tfl
   return pairs * flops_per_pair_d * (double)s.d / (tflops * 1e6);
 }
 
-int fwd_split(const Sizes& s) {
-  const int rows = 32 * fwd_waves(s), keys = fwd_key_tile(s);
-  return split_parts(grid_items(s, rows) * s.hq, tiles_of(s, keys),
-                     tile_us((double)rows * keys, s, 4.0, 4.5),
-                     (double)s.T * s.hq * s.d * 4);
+// sq: the query rows' sizes; sk: the keys' (the same for self-attention
+// over cu's segments, one chunk each for a context-parallel pair)
+int fwd_split(const Sizes& sq, const Sizes& sk) {
+  const int rows = 32 * fwd_waves(sq), keys = fwd_key_tile(sq);
+  return split_parts(grid_items(sq, rows) * sq.hq, tiles_of(sk, keys),
+                     tile_us((double)rows * keys, sq, 4.0, 4.5),
+                     (double)sq.T * sq.hq * sq.d * 4);
 }
 
-int dq_split(const Sizes& s) {
-  const int rows = 32 * fwd_waves(s), keys = dq_key_tile(s);
-  return split_parts(grid_items(s, rows) * s.hq, tiles_of(s, keys),
-                     tile_us((double)rows * keys, s, 6.0, 5.0),
-                     (double)s.T * s.hq * s.d * 4);
+int dq_split(const Sizes& sq, const Sizes& sk) {
+  const int rows = 32 * fwd_waves(sq), keys = dq_key_tile(sq);
+  return split_parts(grid_items(sq, rows) * sq.hq, tiles_of(sk, keys),
+                     tile_us((double)rows * keys, sq, 6.0, 5.0),
+                     (double)sq.T * sq.hq * sq.d * 4);
 }
 
 // the heaviest key tile visits every 64-row query step of every head of its group
-int dkdv_split(const Sizes& s) {
+int dkdv_split(const Sizes& sq, const Sizes& sk) {
   const int rows = pdy::DkdvCfg<128>::BQ;
-  return split_parts(grid_items(s, kTile) * s.hkv, (int64_t)tiles_of(s, rows) * (s.hq / s.hkv),
-                     tile_us((double)rows * kTile, s, 8.0, 4.5),
-                     2.0 * s.T * s.hkv * s.d * 4);
+  return split_parts(grid_items(sk, kTile) * sk.hkv,
+                     (int64_t)tiles_of(sq, rows) * (sq.hq / sq.hkv),
+                     tile_us((double)rows * kTile, sq, 8.0, 4.5),
+                     2.0 * sk.T * sk.hkv * sk.d * 4);
 }
 
 size_t part_o_bytes(const Sizes& s, int p) { return align256((size_t)p * s.T * s.hq * s.d * 4); }
@@ -223,15 +226,15 @@ size_t part_lse_bytes(const Sizes& s, int p) { return align256((size_t)p * s.hq 
 size_t part_kv_bytes(const Sizes& s, int p) { return align256((size_t)p * s.T * s.hkv * s.d * 4); }
 
 // workspace for a split forward's partial O and LSE (none if it is not split)
-size_t fwd_split_bytes(const Sizes& s) {
-  const int p = fwd_split(s);
-  return p > 1 ? part_o_bytes(s, p) + part_lse_bytes(s, p) : 0;
+size_t fwd_split_bytes(const Sizes& sq, const Sizes& sk) {
+  const int p = fwd_split(sq, sk);
+  return p > 1 ? part_o_bytes(sq, p) + part_lse_bytes(sq, p) : 0;
 }
 
-// workspace for a split backward's partial dK, dV and dQ
-size_t bwd_split_bytes(const Sizes& s) {
-  const int pk = dkdv_split(s), pq = dq_split(s);
-  return (pk > 1 ? 2 * part_kv_bytes(s, pk) : 0) + (pq > 1 ? part_o_bytes(s, pq) : 0);
+// workspace for a split backward's partial dK, dV (key rows) and dQ
+size_t bwd_split_bytes(const Sizes& sq, const Sizes& sk) {
+  const int pk = sk.T > 0 ? dkdv_split(sq, sk) : 1, pq = dq_split(sq, sk);
+  return (pk > 1 ? 2 * part_kv_bytes(sk, pk) : 0) + (pq > 1 ? part_o_bytes(sq, pq) : 0);
 }
 
 pdy::Plan make_plan(int32_t* ws, const Sizes& s, int tile) {
@@ -334,7 +337,7 @@ size_t attn_fwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s, 32 * fwd_waves(s)) + fwd_split_bytes(s);
+  return plan_bytes(s, 32 * fwd_waves(s)) + fwd_split_bytes(s, s);
 }
 
 size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv,
@@ -342,7 +345,7 @@ size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
   return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
-         bwd_split_bytes(s);
+         bwd_split_bytes(s, s);
 }
 
 }  // extern "C"
@@ -359,14 +362,18 @@ struct Chunk {
 };
 
 pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu,
-                    const Sizes& s, int32_t causal, float scale, void* o, float* lse,
+                    const Sizes& s, const Sizes& sk, int32_t causal, float scale, void* o,
+                    float* lse,
                     void* workspace, size_t workspace_bytes, void* stream, const Chunk& c,
                     const char* who) {
   pdy_status st;
   const int nw = fwd_waves(s);
   const int tile = 32 * nw;
-  const int nsplit = c.on ? 1 : fwd_split(s);
-  const size_t need = plan_bytes(s, tile) + (nsplit > 1 ? fwd_split_bytes(s) : 0);
+  // a context-parallel pair does not split: the ring already overlaps its
+  // forward calls on two streams, and the backward's partial traffic and
+  // extra launches cancel the gain (measured at 131,072 tokens over p = 8)
+  const int nsplit = c.on ? 1 : fwd_split(s, sk);
+  const size_t need = plan_bytes(s, tile) + (nsplit > 1 ? fwd_split_bytes(s, sk) : 0);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -441,10 +448,10 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   pdy_status st;
   const int nwq = fwd_waves(s);
   const int qtile = 32 * nwq;
-  // split-K only for self-attention over cu's segments (sk is then s)
-  const int nsplit_kv = c.on ? 1 : dkdv_split(s);
-  const int nsplit_q = c.on ? 1 : dq_split(s);
-  const size_t need = bwd_need(s, sk) + (c.on ? 0 : bwd_split_bytes(s));
+  // (no split-K for a context-parallel pair, as in the forward)
+  const int nsplit_kv = c.on || sk.T == 0 ? 1 : dkdv_split(s, sk);
+  const int nsplit_q = c.on ? 1 : dq_split(s, sk);
+  const size_t need = bwd_need(s, sk) + (c.on ? 0 : bwd_split_bytes(s, sk));
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -504,8 +511,8 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     uint8_t* w = reinterpret_cast<uint8_t*>(workspace) + bwd_need(s, sk);
     if (nsplit_kv > 1) {
       a.part_dk = reinterpret_cast<float*>(w);
-      a.part_dv = reinterpret_cast<float*>(w + part_kv_bytes(s, nsplit_kv));
-      w += 2 * part_kv_bytes(s, nsplit_kv);
+      a.part_dv = reinterpret_cast<float*>(w + part_kv_bytes(sk, nsplit_kv));
+      w += 2 * part_kv_bytes(sk, nsplit_kv);
     }
     if (nsplit_q > 1) a.part_dq = reinterpret_cast<float*>(w);
   }
@@ -585,7 +592,7 @@ pdy_status attn_fwd(const void* q, const void* k, const void* v, const int32_t* 
   if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
   if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
     return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
-  return fwd_impl(q, k, v, cu_seqlens, s, causal, scale, o, lse, workspace, workspace_bytes,
+  return fwd_impl(q, k, v, cu_seqlens, s, s, causal, scale, o, lse, workspace, workspace_bytes,
                   stream, Chunk{}, "attn_fwd");
 }
 
@@ -622,7 +629,7 @@ pdy_status attn_fwd_chunk(const void* q, const void* k, const void* v, int32_t t
   c.on = 1;
   c.tk = tk;
   c.shift = q_offset - k_offset;
-  return fwd_impl(q, k, v, nullptr, sq, causal, scale, o, lse, workspace, workspace_bytes, stream,
+  return fwd_impl(q, k, v, nullptr, sq, sk, causal, scale, o, lse, workspace, workspace_bytes, stream,
                   c, "attn_fwd_chunk");
 }
 

@@ -119,7 +119,7 @@ def test_split_k_workspace():
     assert P.bwd_workspace_size(16384, 1, 16384, 8, 8, 64) < 2 * MiB
     # segments of at most 128 tokens leave nothing to split
     assert P.fwd_workspace_size(1024, 8, 128, 1, 1, 64) < MiB
-    # chunk calls never split
+    # context-parallel pair calls never split
     assert P.fwd_chunk_workspace_size(8192, 8192, 4, 4, 128) < MiB
 
 
@@ -190,9 +190,10 @@ def test_chunk_noops_and_workspace_sizes():
     assert _fwd_chunk(tq=0, q=0, k=0, v=0, o=0, lse=0, ws=0, wsb=0) == P.PDY_OK
     assert _bwd_chunk(tq=0, tk=0, q=0, k=0, v=0, o=0, lse=0, do=0, dq=0, dk=0, dv=0, ws=0,
                       wsb=0) == P.PDY_OK
-    f = P.fwd_chunk_workspace_size(4096, 8192, 4, 4, 128)
-    b = P.bwd_chunk_workspace_size(4096, 8192, 4, 4, 128)
-    assert 256 <= f < 1 << 20 and b >= 4 * 4096 * 4
+    # a pair that fills the chip needs only the schedule (and D for the backward)
+    f = P.fwd_chunk_workspace_size(32768, 65536, 32, 8, 128)
+    b = P.bwd_chunk_workspace_size(32768, 65536, 32, 8, 128)
+    assert 256 <= f < 1 << 20 and 32 * 32768 * 4 <= b < 32 * 32768 * 4 + (1 << 20)
     assert P.fwd_chunk_workspace_size(-1, 5, 4, 4, 128) == 0
     L = P.lib()
     assert L.attn_merge(FAKE, FAKE, FAKE, FAKE, 10, 4, 96, FAKE, FAKE, None) == P.PDY_ERR_UNSUPPORTED
