@@ -352,10 +352,10 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   };
   auto rows_valid = [&](const StepPos& p) __attribute__((always_inline)) { return q_hi - p.r0; };
 
-  // K and V tiles: keys past the segment end read as zeros (d = 128 copies)
-  // or repeat the last key (d = 64 loads); their gradients are never written
-  // out.  Query-side rows past the segment end likewise, and are masked.
-  if constexpr (D == 128) {
+  // K and V tiles: keys past the segment end read as zeros (the copies'
+  // range check); their gradients are never written out.  Query-side rows
+  // past the segment end likewise, and are masked.
+  {
     {
       TileDma<KL, BK, NW> kvd;
       kvd.init(kvstride);
@@ -402,39 +402,6 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
         }
       });
       if (!ran && more) issue(step + 1, nxt);
-      cur = nxt;
-    }
-  } else {
-    {
-      TileLoader<KL, BK, D, C::NT> kl, vl;
-      kl.load_clamped(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0);
-      vl.load_clamped(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0);
-      kl.store(ktile_s);
-      vl.store(vtile);
-    }
-    TileLoader<QL, BQ, D, C::NT> ql, gl;
-    auto issue = [&](const StepPos& p) __attribute__((always_inline)) {
-      ql.load_clamped(row_ptr(a.q, p), qstride, rows_valid(p));
-      gl.load_clamped(row_ptr(a.dout, p), qstride, rows_valid(p));
-      load_stat(p);
-    };
-    auto commit = [&](int b) __attribute__((always_inline)) {
-      ql.store(qbuf(b));
-      gl.store(gbuf(b));
-      store_stat(b);
-    };
-    StepPos cur = first;
-    if (nsteps > 0) {
-      issue(cur);
-      commit(0);
-    }
-    for (int step = 0; step < nsteps; ++step) {
-      const bool more = step + 1 < nsteps;
-      const StepPos nxt = advance(cur);
-      if (more) issue(nxt);
-      __syncthreads();
-      compute(step, cur, no_hook);
-      if (more) commit((step + 1) & 1);
       cur = nxt;
     }
   }
@@ -638,9 +605,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
     return true;
   };
 
-  // keys past the segment end read as zeros (d = 128 copies) or repeat the
-  // last key (d = 64 loads); they are always masked
-  if constexpr (D == 128) {
+  // keys past the segment end read as zeros (the copies' range check); they
+  // are always masked
+  {
     using KD = TileDma<KL, BK, NW>;
     using VD = TileDma<VL, BK, NW>;
     // the next tile's copies go out one every GAP K-steps of S^T/dP^T rather
@@ -677,30 +644,6 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
         }
       });
       if (!ran && more) issue(it + 1);
-    }
-  } else {
-    TileLoader<KL, BK, D, C::NT> kl;
-    TileLoader<VL, BK, D, C::NT> vl;
-    if (t_begin < t_end) {
-      const int k1 = k_lo + t_begin * BK;
-      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-      kl.store(kbuf(t_begin));
-      vl.store(vbuf(t_begin));
-    }
-    for (int it = t_begin; it < t_end; ++it) {
-      const bool more = it + 1 < t_end;
-      if (more) {
-        const int k1 = k_lo + (it + 1) * BK;
-        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-      }
-      __syncthreads();
-      compute(it, [](auto) {});
-      if (more) {
-        kl.store(kbuf(it + 1));
-        vl.store(vbuf(it + 1));
-      }
     }
   }
 

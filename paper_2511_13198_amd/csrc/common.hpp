@@ -239,44 +239,9 @@ __device__ __forceinline__ void row_wait(u32x4& a, u32x4& b, u32x4& c, u32x4& d)
 }
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& r) { return __builtin_bit_cast(bf16x8, r); }
 
-// Cooperative copy of a [ROWS x D] bf16 tile (rows of global stride `gstride`
-// elements) through registers into layout L: NT threads, 16 B per thread per
-// step.  Used where direct copies do not apply (D = 64).
-template <class L, int ROWS, int D, int NT>
-struct TileLoader {
-  static constexpr int CHUNKS_PER_ROW = D / 8;
-  static constexpr int TOTAL = ROWS * CHUNKS_PER_ROW;
-  static constexpr int STEPS = TOTAL / NT;
-  static_assert(TOTAL % NT == 0, "tile must split evenly over the workgroup");
-  u32x4 regs[STEPS];
-
-  // Rows >= valid_rows (valid_rows >= 1) repeat the last valid row: callers
-  // mask them (their probabilities are exactly zero).
-  __device__ __forceinline__ void load_clamped(const uint16_t* base, size_t gstride,
-                                               int valid_rows) {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      const int c = t + s * NT;
-      int row = c / CHUNKS_PER_ROW;
-      row = row < valid_rows ? row : valid_rows - 1;
-      const int col = (c % CHUNKS_PER_ROW) * 8;
-      regs[s] = *reinterpret_cast<const u32x4*>(base + (size_t)row * gstride + col);
-    }
-  }
-  __device__ __forceinline__ void store(uint16_t* lds) const {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      const int c = t + s * NT;
-      *reinterpret_cast<u32x4*>(lds + L::off(c / CHUNKS_PER_ROW, c % CHUNKS_PER_ROW)) = regs[s];
-    }
-  }
-};
-
 // Direct global -> LDS copy (buffer_load_dwordx4 ... lds: no registers, no LDS
-// store instructions) of a [ROWS x 128] bf16 tile into layout L.  One
-// instruction moves 64 lanes x 16 B into 1 KB of consecutive LDS (lane l at
+// store instructions) of a [ROWS x D] bf16 tile (D = 64 or 128) into layout
+// L.  One instruction moves 64 lanes x 16 B into 1 KB of consecutive LDS (lane l at
 // base + 16 l, the base in M0); lane l of instruction k therefore fills 16-byte
 // slot 64 k + l of the tile and fetches whichever global chunk the layout
 // stores there.  The copies read through a buffer resource over the tile's

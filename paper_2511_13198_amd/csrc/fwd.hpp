@@ -11,9 +11,9 @@
 // The probabilities are rounded to bf16 and fed back as the B operand of
 //   O^T += V^T P^T          (32 head-dim x 32 rows per MFMA tile)
 // with V^T read from the row-major LDS tile by transposing reads.  K/V tiles
-// (128 keys at d = 128 with 8 waves, else 64) reach LDS by direct copies
-// (d = 128) or through registers (d = 64); tile t+1 is in flight while tile t
-// is computed, in softmax steps of 64 keys.  Tiles entirely above the causal
+// (128 keys at d = 128 with 8 waves, else 64) reach LDS by direct copies;
+// tile t+1 is in flight while tile t is computed, in softmax steps of 64
+// keys.  Tiles entirely above the causal
 // diagonal are never visited; only tiles crossing the diagonal or the segment
 // end are masked.  When a launch has too few query tiles to fill the chip, a
 // workgroup takes one contiguous part of its query tile's key tiles (split-K)
@@ -51,9 +51,8 @@ struct FwdCfg {
   using VL = DualLayout<D>;  // V is only read transposed
   static constexpr int KTILE = KL::elems(BK);
   static constexpr int VTILE = VL::elems(BK);
-  // K/V tiles in flight: direct copies run STAGES-1 tiles ahead (d = 128);
-  // the register-staged path (d = 64) double-buffers
-  static constexpr int STAGES = (D == 128) ? PDY_FWD_STAGES : 2;
+  // K/V tiles in flight: the direct copies run STAGES-1 tiles ahead
+  static constexpr int STAGES = PDY_FWD_STAGES;
   static constexpr int LDS_BYTES = STAGES * (KTILE + VTILE) * 2;
 };
 
@@ -264,9 +263,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
   auto no_hook = [](auto) {};
-  // keys past the segment end read as zeros (d = 128 copies) or repeat the
-  // last key (d = 64 loads); they are always masked
-  if constexpr (D == 128) {
+  // keys past the segment end read as zeros (the copies' range check); they
+  // are always masked
+  {
     // K/V tiles land in LDS by direct copies, no staging registers
     TileDma<KL, BK, NW> kd;
     TileDma<VL, BK, NW> vd;
@@ -329,33 +328,6 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
         });
       } else if (more) {
         issue(tn);
-      }
-    }
-  } else {
-    TileLoader<KL, BK, D, C::NT> kl;
-    TileLoader<VL, BK, D, C::NT> vl;
-    if (t_begin < t_end) {
-      const int k1 = k_lo + t_begin * BK;
-      kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-      vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-      kl.store(kbuf(t_begin));
-      vl.store(vbuf(t_begin));
-    }
-    for (int it = t_begin; it < t_end; ++it) {
-      const bool more = it + 1 < t_end;
-      if (more) {
-        const int k1 = k_lo + (it + 1) * BK;
-        kl.load_clamped(kbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-        vl.load_clamped(vbase + (size_t)k1 * kvstride, kvstride, k_hi - k1);
-      }
-      __syncthreads();
-      if (active(it)) {
-        compute_s(kbuf(it), no_hook);
-        softmax_pv(k_lo + it * BK, vbuf(it));
-      }
-      if (more) {
-        kl.store(kbuf(it + 1));
-        vl.store(vbuf(it + 1));
       }
     }
   }
