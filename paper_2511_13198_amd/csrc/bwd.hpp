@@ -450,7 +450,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
 template <int D, int NW>
 struct DqCfg {
   static constexpr int BQ = 32 * NW;
-  static constexpr int BK = (D == 128 && NW == 8) ? PDY_DQ_BK : 64;  // keys per tile
+  static constexpr int BK = (NW == 8) ? PDY_DQ_BK : 64;  // keys per tile
   static constexpr int NT = NW * 64;
   using KL = DualLayout<D>;  // K is read as rows (S^T) and transposed (dQ^T)
   using VL = RowsLayout<D>;  // V is read as rows (dP^T)
