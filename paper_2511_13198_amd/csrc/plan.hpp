@@ -28,29 +28,38 @@ __host__ __device__ inline size_t plan_ints(int n, int max_nt) {
 
 // In-place suffix sum over a[0..n) by the whole workgroup: a[j] becomes
 // sum_{j' >= j} a[j'] (inclusive) or sum_{j' > j} a[j'] (exclusive).  Each
-// thread owns a chunk of consecutive entries counted from the top; thread 0
-// scans the per-thread totals in `part`.  Returns the sum of all entries.
-__device__ inline int suffix_sum(int32_t* a, int n, bool inclusive, int32_t* part) {
+// thread owns a chunk of consecutive entries counted from the top; the
+// threads' totals are scanned within each wave by shuffles and across the
+// waves by thread 0 over the wave totals in `wsum` (kPlanThreads / 64 + 1
+// entries).  Returns the sum of all entries.
+__device__ inline int suffix_sum(int32_t* a, int n, bool inclusive, int32_t* wsum) {
   const int t = threadIdx.x;
+  const int lane = t & 63, wv = t >> 6;
+  constexpr int kWaves = kPlanThreads / 64;
   const int chunk = (n + kPlanThreads - 1) / kPlanThreads;
   int local = 0;
   for (int c = 0; c < chunk; ++c) {
     const int idx = t * chunk + c;
     if (idx < n) local += a[n - 1 - idx];
   }
-  part[t] = local;
+  int incl = local;  // inclusive scan of the threads' totals within the wave
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) wsum[wv] = incl;
   __syncthreads();
   if (t == 0) {
     int run = 0;
-    for (int i = 0; i < kPlanThreads; ++i) {
-      const int v = part[i];
-      part[i] = run;
+    for (int w = 0; w < kWaves; ++w) {
+      const int v = wsum[w];
+      wsum[w] = run;
       run += v;
     }
-    part[kPlanThreads] = run;
+    wsum[kWaves] = run;
   }
   __syncthreads();
-  int run = part[t];
+  int run = wsum[wv] + incl - local;  // the totals of all earlier threads
   for (int c = 0; c < chunk; ++c) {
     const int idx = t * chunk + c;
     if (idx < n) {
@@ -61,7 +70,7 @@ __device__ inline int suffix_sum(int32_t* a, int n, bool inclusive, int32_t* par
       if (!inclusive) run += v;
     }
   }
-  const int total = part[kPlanThreads];
+  const int total = wsum[kWaves];
   __syncthreads();
   return total;
 }
@@ -76,7 +85,7 @@ plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int singl
   int32_t* start = cnt + max_nt;
   int32_t* total = start + max_nt;
   const int t = threadIdx.x;
-  __shared__ int32_t part[kPlanThreads + 1];
+  __shared__ int32_t wsum[kPlanThreads / 64 + 1];
   // per-count histogram and placement cursors: in LDS when they fit (many
   // segments with the same count then contend in LDS, not in L2)
   __shared__ int32_t lds_hist[kLdsBuckets];
@@ -105,7 +114,7 @@ plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int singl
     for (int j = t; j < max_nt; j += kPlanThreads) cnt[j] = hist[j];
     __syncthreads();
   }
-  suffix_sum(cnt, max_nt, true, part);
+  suffix_sum(cnt, max_nt, true, wsum);
 
   // 3. order: segments by tile count, most first (a counting sort: the ones
   // with v tiles fill positions [cnt[v], cnt[v - 1]) through the per-count
@@ -121,7 +130,7 @@ plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int singl
   // 4. start[j] = sum_{j' > j} cnt[j'] (first item of level j); total items
   for (int j = t; j < max_nt; j += kPlanThreads) start[j] = cnt[j];
   __syncthreads();
-  const int items = suffix_sum(start, max_nt, false, part);
+  const int items = suffix_sum(start, max_nt, false, wsum);
   if (t == 0) *total = items;
 }
 
