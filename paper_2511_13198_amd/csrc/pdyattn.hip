@@ -304,13 +304,20 @@ pdy_status check_ptr(const void* p, const char* name) {
   return PDY_OK;
 }
 
-// cu == nullptr: one segment of s.T tokens
-pdy_status launch_plan(const int32_t* cu, int32_t* ws, const Sizes& s, int tile,
-                       hipStream_t st) {
-  const int nt = tiles_of(s, tile);
+// The schedule of s's segments in tiles of `tile` (cu == nullptr: one segment
+// of s.T tokens), written to ws
+pdy::PlanJob plan_job(const int32_t* cu, int32_t* ws, const Sizes& s, int tile) {
+  return pdy::PlanJob{cu, (int)s.N, tile, tiles_of(s, tile), (int)s.T, ws};
+}
+
+// one or two schedules in one launch
+pdy_status launch_plans(const pdy::PlanJob& a, const pdy::PlanJob* b, hipStream_t st) {
+  pdy::PlanJobs jobs;
+  jobs.job[0] = a;
+  jobs.job[1] = b ? *b : a;
+  const dim3 grid(b ? 2 : 1);
   hipError_t e = launch_timed(K_PLAN, st, [&] {
-    hipLaunchKernelGGL(pdy::plan_kernel, dim3(1), dim3(pdy::kPlanThreads), 0, st, cu, (int)s.N,
-                       tile, nt, (int)s.T, ws);
+    hipLaunchKernelGGL(pdy::plan_kernel, grid, dim3(pdy::kPlanThreads), 0, st, jobs);
   });
   if (e != hipSuccess) return hip_fail(e, "plan_kernel launch");
   return PDY_OK;
@@ -381,7 +388,7 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
   if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   int32_t* ws = reinterpret_cast<int32_t*>(workspace);
-  if ((st = launch_plan(cu, ws, s, tile, hs)) != PDY_OK) return st;
+  if ((st = launch_plans(plan_job(cu, ws, s, tile), nullptr, hs)) != PDY_OK) return st;
 
   pdy::FwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
@@ -464,8 +471,12 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) +
                                        plan_bytes(sk, kTile) + plan_bytes(s, qtile));
 
-  if (sk.T > 0 && (st = launch_plan(cu, ws, sk, kTile, hs)) != PDY_OK) return st;
-  if ((st = launch_plan(cu, ws_q, s, qtile, hs)) != PDY_OK) return st;
+  {
+    // the query-tile schedule, and the key-tile one unless there are no keys
+    const pdy::PlanJob q_job = plan_job(cu, ws_q, s, qtile);
+    const pdy::PlanJob kv_job = plan_job(cu, ws, sk, kTile);
+    if ((st = launch_plans(q_job, sk.T > 0 ? &kv_job : nullptr, hs)) != PDY_OK) return st;
+  }
   {
     const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
     const unsigned blocks = (unsigned)((threads + 255) / 256);

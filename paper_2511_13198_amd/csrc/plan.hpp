@@ -75,10 +75,25 @@ __device__ inline int suffix_sum(int32_t* a, int n, bool inclusive, int32_t* wsu
   return total;
 }
 
-// cu == nullptr: a single segment of single_len tokens (n must be 1)
-__global__ void __launch_bounds__(kPlanThreads)
-plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int single_len,
-            int32_t* __restrict__ ws) {
+// One schedule to build: segments from cu (cu == nullptr: a single segment
+// of single_len tokens, n must be 1), tiles of bt tokens, at most max_nt per
+// segment, written to ws.
+struct PlanJob {
+  const int32_t* cu;
+  int n;
+  int bt;
+  int max_nt;
+  int single_len;
+  int32_t* ws;
+};
+// Up to two schedules per launch (the backward needs one over key tiles and
+// one over query tiles): workgroup b builds job[b].
+struct PlanJobs {
+  PlanJob job[2];
+};
+
+__device__ inline void build_plan(const int32_t* __restrict__ cu, int n, int bt, int max_nt,
+                                  int single_len, int32_t* __restrict__ ws) {
   int32_t* nt = ws;
   int32_t* order = nt + n;
   int32_t* cnt = order + n;
@@ -132,6 +147,11 @@ plan_kernel(const int32_t* __restrict__ cu, int n, int bt, int max_nt, int singl
   __syncthreads();
   const int items = suffix_sum(start, max_nt, false, wsum);
   if (t == 0) *total = items;
+}
+
+__global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanJobs jobs) {
+  const PlanJob& j = jobs.job[blockIdx.x];
+  build_plan(j.cu, j.n, j.bt, j.max_nt, j.single_len, j.ws);
 }
 
 }  // namespace pdy
