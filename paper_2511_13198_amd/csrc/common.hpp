@@ -333,7 +333,8 @@ __device__ __forceinline__ void wait_dma_n() {
 // (dK/dV); items are ordered by descending level so the heaviest causal tiles
 // start first.  Returns false when `item` is past the end.
 struct Plan {
-  const int32_t* order;  // segments sorted by tile count, descending [N]
+  const int32_t* order;  // segments sorted by tile count, descending [N];
+                         // null: a single segment of max_nt tiles (no schedule)
   const int32_t* start;  // first item of each level [max_nt]
   const int32_t* total;  // number of items [1]
   int32_t max_nt;
@@ -351,8 +352,8 @@ struct Plan {
 // always gets the lightest block; with 8 heads this is the plain order).
 // Measured at 131,072 tokens: dK/dV with 1 kv head -4.7 %, 2 kv heads
 // -3.9 %, 4 kv heads -0.3 to -0.8 %; forward and dQ with 4 query heads
-// -1.4 % and -0.6 %.  Other head counts keep the plain order.  A bijection on [0, n); the last partial round keeps the
-// plain order.
+// -1.4 % and -0.6 %.  Other head counts keep the plain order.  A bijection
+// on [0, n); the last partial round keeps the plain order.
 __device__ __forceinline__ void xcd_order(int b, int n, int nheads, int& head, int& entry) {
   constexpr int kXcd = 8, kPer = 32, kRound = kXcd * kPer;
   head = b % nheads;
@@ -367,6 +368,12 @@ __device__ __forceinline__ void xcd_order(int b, int n, int nheads, int& head, i
 }
 
 __device__ __forceinline__ bool plan_lookup(const Plan& p, int item, int& seg, int& level) {
+  if (p.order == nullptr) {  // one segment: item i is its level max_nt - 1 - i
+    if (item >= p.max_nt) return false;
+    seg = 0;
+    level = p.max_nt - 1 - item;
+    return true;
+  }
   if (item >= *p.total) return false;
   // smallest j with start[j] <= item (start is non-increasing in j)
   int lo = 0, hi = p.max_nt - 1;

@@ -237,9 +237,18 @@ size_t bwd_split_bytes(const Sizes& sq, const Sizes& sk) {
   return (pk > 1 ? 2 * part_kv_bytes(sk, pk) : 0) + (pq > 1 ? part_o_bytes(sq, pq) : 0);
 }
 
+// A single segment (N = 1: by the contract cu = [0, T], and max_seqlen = T)
+// needs no schedule: item i is its level nt - 1 - i, so no plan is built.
+bool needs_plan(const Sizes& s) { return s.N > 1; }
+
 pdy::Plan make_plan(int32_t* ws, const Sizes& s, int tile) {
   const int nt = tiles_of(s, tile);
   pdy::Plan p;
+  if (!needs_plan(s)) {
+    p.order = p.start = p.total = nullptr;
+    p.max_nt = nt;
+    return p;
+  }
   p.order = ws + s.N;
   p.start = ws + 2 * s.N + nt;
   p.total = ws + 2 * s.N + 2 * nt;
@@ -388,7 +397,8 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
   if (e != hipSuccess) return hip_fail(e, "kernel attribute setup");
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   int32_t* ws = reinterpret_cast<int32_t*>(workspace);
-  if ((st = launch_plans(plan_job(cu, ws, s, tile), nullptr, hs)) != PDY_OK) return st;
+  if (needs_plan(s) && (st = launch_plans(plan_job(cu, ws, s, tile), nullptr, hs)) != PDY_OK)
+    return st;
 
   pdy::FwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
@@ -473,9 +483,12 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
 
   {
     // the query-tile schedule, and the key-tile one unless there are no keys
+    // (the key side has the same segments as the query side, or is a chunk)
     const pdy::PlanJob q_job = plan_job(cu, ws_q, s, qtile);
     const pdy::PlanJob kv_job = plan_job(cu, ws, sk, kTile);
-    if ((st = launch_plans(q_job, sk.T > 0 ? &kv_job : nullptr, hs)) != PDY_OK) return st;
+    if (needs_plan(s) &&
+        (st = launch_plans(q_job, sk.T > 0 ? &kv_job : nullptr, hs)) != PDY_OK)
+      return st;
   }
   {
     const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
