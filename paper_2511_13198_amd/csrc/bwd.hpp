@@ -23,13 +23,25 @@
 namespace pdy {
 
 // dst = (accumulate ? dst : 0) + sum_p parts[p * n + i] over the nsplit
-// partial gradients of a split-K backward, in part order; 4 floats per
-// thread (n is a multiple of 4: a head dimension of 64 or 128 divides it).
-__global__ void __launch_bounds__(256) split_sum_kernel(const float* __restrict__ parts,
-                                                        int nsplit, size_t n,
-                                                        float* __restrict__ dst, int accumulate) {
-  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i >= n) return;
+// partial gradients of a split-K backward, in part order, for one array
+// (parts_b == nullptr) or two of the same size (dK and dV in one launch:
+// the grid's second half takes the second); 4 floats per thread (n is a
+// multiple of 4: a head dimension of 64 or 128 divides it).
+__global__ void __launch_bounds__(256) split_sum_kernel(const float* __restrict__ parts_a,
+                                                        float* __restrict__ dst_a,
+                                                        const float* __restrict__ parts_b,
+                                                        float* __restrict__ dst_b, int nsplit,
+                                                        size_t n, int accumulate) {
+  size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  const float* parts = parts_a;
+  float* dst = dst_a;
+  if (i >= n) {
+    if (parts_b == nullptr) return;
+    i -= n;
+    if (i >= n) return;
+    parts = parts_b;
+    dst = dst_b;
+  }
   f32x4 acc = accumulate ? *reinterpret_cast<const f32x4*>(dst + i) : f32x4{0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < nsplit; ++p) acc += *reinterpret_cast<const f32x4*>(parts + p * n + i);
   *reinterpret_cast<f32x4*>(dst + i) = acc;

@@ -540,12 +540,14 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     }
     if (nsplit_q > 1) a.part_dq = reinterpret_cast<float*>(w);
   }
-  // the parts' partial gradients, summed into dst
-  auto sum_parts = [&](const float* parts, int nsplit, size_t n, float* dst) {
-    const dim3 blocks((unsigned)((n / 4 + 255) / 256));
+  // the parts' partial gradients, summed into dst (and parts_b into dst_b)
+  auto sum_parts = [&](const float* parts, float* dst, const float* parts_b, float* dst_b,
+                       int nsplit, size_t n) {
+    const size_t threads = (parts_b ? 2 : 1) * (n / 4);
+    const dim3 blocks((unsigned)((threads + 255) / 256));
     return launch_timed(K_SPLIT_SUM, hs, [&] {
-      hipLaunchKernelGGL(pdy::split_sum_kernel, blocks, dim3(256), 0, hs, parts, nsplit, n, dst,
-                         c.accumulate);
+      hipLaunchKernelGGL(pdy::split_sum_kernel, blocks, dim3(256), 0, hs, parts, dst, parts_b,
+                         dst_b, nsplit, n, c.accumulate);
     });
   };
   if (sk.T > 0) {
@@ -561,8 +563,7 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
     if (nsplit_kv > 1) {
       const size_t n = (size_t)sk.T * s.hkv * s.d;
-      if ((e = sum_parts(a.part_dk, nsplit_kv, n, dk)) != hipSuccess ||
-          (e = sum_parts(a.part_dv, nsplit_kv, n, dv)) != hipSuccess)
+      if ((e = sum_parts(a.part_dk, dk, a.part_dv, dv, nsplit_kv, n)) != hipSuccess)
         return hip_fail(e, "split_sum_kernel launch");
     }
   }
@@ -578,7 +579,8 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   });
   if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
   if (nsplit_q > 1 &&
-      (e = sum_parts(a.part_dq, nsplit_q, (size_t)s.T * s.hq * s.d, dq)) != hipSuccess)
+      (e = sum_parts(a.part_dq, dq, nullptr, nullptr, nsplit_q, (size_t)s.T * s.hq * s.d)) !=
+          hipSuccess)
     return hip_fail(e, "split_sum_kernel launch");
   return PDY_OK;
 }

@@ -205,11 +205,11 @@ def test_single_131072_h4():
 # Launches too small to fill 256 CUs split each work item's inner loop into
 # parts (split-K): forward and dQ by key tiles, dK/dV by query steps.  The
 # expected combining launches follow from the sizes: one forward merge when
-# the forward splits, one sum for dQ, two (dK, dV) for dK/dV.
+# the forward splits, one sum for dQ and one for dK and dV together.
 @pytest.mark.parametrize("lengths,hq,hkv,d,expect", [
-    ([8192], 4, 4, 128, {"merge": 1, "sum": 3}),        # forward/dQ in 4 parts, dK/dV in 2
-    ([16384], 8, 2, 128, {"merge": 0, "sum": 2}),       # only dK/dV (grouped heads) splits
-    ([3000, 5000, 77], 2, 1, 64, {"merge": 1, "sum": 3}),  # packed, d = 64, 4 parts each
+    ([8192], 4, 4, 128, {"merge": 1, "sum": 2}),        # forward/dQ in 4 parts, dK/dV in 2
+    ([16384], 8, 2, 128, {"merge": 0, "sum": 1}),       # only dK/dV (grouped heads) splits
+    ([3000, 5000, 77], 2, 1, 64, {"merge": 1, "sum": 2}),  # packed, d = 64, 4 parts each
     ([16384], 8, 8, 64, {"merge": 0, "sum": 0}),        # fills the chip: no split
 ])
 def test_split_k(lengths, hq, hkv, d, expect):
