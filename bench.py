@@ -112,7 +112,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, "
-              f"WORLD_SIZE={world}); multi-GPU runs are not part of this build",
+              f"WORLD_SIZE={world}): the library computes one GPU's share of the "
+              f"attention, and sharding it over several GPUs is not implemented",
               file=sys.stderr)
         sys.exit(2)
 

@@ -68,3 +68,16 @@ def test_host_inputs_deterministic():
     assert a["q"].shape == (100, 4, 16) and a["k"].shape == (100, 2, 16)
     x = wl.bf16_bits_to_f64(a["q"])
     assert abs(x.mean()) < 0.1 and abs(x.std() - 1) < 0.1
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: asked for more it exits with status 2 and a
+    message, before touching a GPU."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr and r.stdout == ""
