@@ -23,7 +23,9 @@
  *     cu[0] = 0, cu[i] <= cu[i+1], cu[num_seqs] = total_tokens.  Zero-length
  *     segments are allowed.  Its contents are trusted (reading them on the
  *     host would force a synchronisation); attn_validate_cu_seqlens checks it.
- *   - max_seqlen must be >= every segment length (an upper bound suffices).
+ *   - max_seqlen must be >= every segment length (an upper bound suffices);
+ *     with num_seqs = 1 it must equal total_tokens (the one segment is
+ *     [0, T)), else the call returns PDY_ERR_INVALID_ARG.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream) and
  *     the call returns without synchronising.  Outputs are fully overwritten.
  *   - Argument errors are reported before anything is launched.  A non-OK

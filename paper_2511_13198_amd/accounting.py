@@ -36,16 +36,27 @@ def fwd_bwd_flops(lengths, heads_q, head_dim, causal=True) -> float:
     return 3.5 * fwd_flops(lengths, heads_q, head_dim, causal)
 
 
-# Algorithmic FLOPs of each kernel of the library (matrix products it is
-# required to perform per visible pair, 2*d each):
-#   fwd_kernel      S, PV                -> 2 products
-#   bwd_dkdv_kernel S, dP, dV, dK        -> 4 products
-#   bwd_dq_kernel   S, dP, dQ            -> 3 products (S and dP recomputed)
-KERNEL_PRODUCTS = {"fwd_kernel": 2, "bwd_dkdv_kernel": 4, "bwd_dq_kernel": 3}
+# Algorithmic FLOPs of each kernel: the matrix products of the method it
+# accounts for, 2*d per visible pair each.  The dQ kernel's share of the
+# gradient is the single product dQ = scale * dS K; it also recomputes S and
+# dP (which the dK/dV kernel already formed), and those are issued work, not
+# algorithmic work:
+#   fwd_kernel      S, PV                -> 2 products (issued 2)
+#   bwd_dkdv_kernel S, dP, dV, dK        -> 4 products (issued 4)
+#   bwd_dq_kernel   dQ                   -> 1 product  (issued 3: S, dP, dQ)
+KERNEL_PRODUCTS = {"fwd_kernel": 2, "bwd_dkdv_kernel": 4, "bwd_dq_kernel": 1}
+ISSUED_PRODUCTS = {"fwd_kernel": 2, "bwd_dkdv_kernel": 4, "bwd_dq_kernel": 3}
 
 
 def kernel_flops(kernel: str, lengths, heads_q, head_dim, causal=True) -> float:
+    """Algorithmic FLOPs of one launch of `kernel` (visible pairs only)."""
     return KERNEL_PRODUCTS[kernel] * 2.0 * head_dim * heads_q * pairs_per_head(lengths, causal)
+
+
+def kernel_issued_flops(kernel: str, lengths, heads_q, head_dim, causal=True) -> float:
+    """Matrix-product FLOPs the kernel issues on visible pairs, recomputation
+    included (masked halves of diagonal tiles still not counted)."""
+    return ISSUED_PRODUCTS[kernel] * 2.0 * head_dim * heads_q * pairs_per_head(lengths, causal)
 
 
 def fwd_bytes(total_tokens, heads_q, heads_kv, head_dim) -> float:

@@ -357,7 +357,6 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     __builtin_amdgcn_s_setprio(0);
     return true;
   };
-  auto no_hook = [](auto) {};
 
   auto row_ptr = [&](const uint16_t* t, const StepPos& p) __attribute__((always_inline)) {
     return t + (size_t)p.r0 * qstride + (size_t)p.h * D;
@@ -418,7 +417,11 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     }
   }
 
-  // sum the pair's accumulators: waves 4..7 park theirs in LDS
+  // sum the pair's accumulators: waves 4..7 park theirs in LDS, over the
+  // K/V and Q/dO tiles.  Every copy this wave issued must have landed first
+  // (a part with no query steps still issued its K/V copies), then the
+  // barrier orders the other waves' copies and reads before the stores.
+  wait_dma();
   __syncthreads();
   float* red = reinterpret_cast<float*>(base) + pw * (32 * D * 2);
   if (half == 1) {

@@ -262,7 +262,6 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
 
   const uint16_t* kbase = a.k + (size_t)hk * D;
   const uint16_t* vbase = a.v + (size_t)hk * D;
-  auto no_hook = [](auto) {};
   // keys past the segment end read as zeros (the copies' range check); they
   // are always masked
   {

@@ -59,6 +59,12 @@ pdy_status check_sizes(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t
                 maxlen, T);
   if (T > 0 && maxlen < 1)
     return fail(PDY_ERR_INVALID_ARG, "max_seqlen must be >= 1 when total_tokens > 0");
+  // one segment spans [0, T) by the contract, and a single-segment call
+  // builds no tile schedule but sizes its grid from max_seqlen: anything
+  // other than T would leave rows unwritten (or visit rows past the end)
+  if (N == 1 && maxlen != T)
+    return fail(PDY_ERR_INVALID_ARG,
+                "with num_seqs = 1 max_seqlen must equal total_tokens (got %d, T=%d)", maxlen, T);
   if (hq < 1 || hkv < 1)
     return fail(PDY_ERR_INVALID_ARG, "head counts must be >= 1 (got Hq=%d, Hkv=%d)", hq, hkv);
   if (hq % hkv != 0)

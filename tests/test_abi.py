@@ -58,6 +58,8 @@ def _bwd(**kw):
     (dict(T=-1), P.PDY_ERR_INVALID_ARG, "total_tokens"),
     (dict(maxlen=513), P.PDY_ERR_INVALID_ARG, "max_seqlen"),
     (dict(maxlen=0), P.PDY_ERR_INVALID_ARG, "max_seqlen"),
+    # one segment is [0, T): a smaller bound would leave rows unwritten
+    (dict(maxlen=500), P.PDY_ERR_INVALID_ARG, "num_seqs = 1"),
     (dict(causal=2), P.PDY_ERR_INVALID_ARG, "causal"),
     (dict(scale=0.0), P.PDY_ERR_INVALID_ARG, "scale"),
     (dict(scale=float("nan")), P.PDY_ERR_INVALID_ARG, "scale"),
@@ -79,6 +81,7 @@ def test_fwd_argument_errors(kw, status, msg):
     (dict(do=FAKE + 4), P.PDY_ERR_INVALID_ARG, "aligned"),
     (dict(wsb=1024), P.PDY_ERR_WORKSPACE, "workspace"),
     (dict(hq=32, hkv=5), P.PDY_ERR_INVALID_ARG, "multiple"),
+    (dict(maxlen=1), P.PDY_ERR_INVALID_ARG, "num_seqs = 1"),
 ])
 def test_bwd_argument_errors(kw, status, msg):
     st = _bwd(**kw)
