@@ -6,4 +6,4 @@ definition of Eq. (2) (section 3) and its calculus gradient; see
 oracle/attention.py for the readings taken where the paper is silent.
 """
 from .attention import (forward, backward, rows_forward_backward, cols_backward,  # noqa: F401
-                        segments)
+                        head_rows, key_window_backward, segments)

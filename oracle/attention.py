@@ -213,6 +213,76 @@ def cols_backward(q, k, v, do, cu_seqlens, causal: bool, scale: float,
     return out
 
 
+def head_rows(q, k, v, do, cu_seqlens, causal: bool, scale: float, h: int, r_lo: int,
+              r_hi: int, row_block: int = 256):
+    """O_i, LSE_i, D_i = <dO_i, O_i> and dQ_i of query head h for every row
+    r_lo <= i < r_hi (any range; rows take the keys of their own segment).
+    Each block of rows is the full definition over all the keys it sees, as
+    in backward(), so a range covering a whole segment is that segment's
+    complete forward plus the dQ part of its gradient.  Inputs as for
+    rows_forward_backward.  Returns (o [n, d], lse [n], dd [n], dq [n, d])."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    Hq, Hkv = _nheads(q), _nheads(k)
+    hk = h // (Hq // Hkv)
+    qh, kh, vh, doh = _head(q, h), _head(k, hk), _head(v, hk), _head(do, h)
+    n = r_hi - r_lo
+    o = np.zeros((n, vh.shape[1]))
+    lse = np.zeros(n)
+    dd = np.zeros(n)
+    dq = np.zeros((n, qh.shape[1]))
+    for si in range(len(cu) - 1):
+        a, b = int(cu[si]), int(cu[si + 1])
+        for r0 in range(max(a, r_lo), min(b, r_hi), row_block):
+            r1 = min(b, r_hi, r0 + row_block)
+            nk = _visible_keys(a, b, r0, r1, causal)
+            kk, vv = kh[a:a + nk], vh[a:a + nk]
+            s = _logits(qh[r0:r1], kk, a, r0, causal, scale)
+            l, p = _softmax_stats(s)
+            orow = p @ vv
+            dor = doh[r0:r1]
+            D = np.sum(dor * orow, axis=1)
+            ds = p * (dor @ vv.T - D[:, None])
+            sl = slice(r0 - r_lo, r1 - r_lo)
+            o[sl], lse[sl], dd[sl], dq[sl] = orow, l, D, scale * (ds @ kk)
+    return o, lse, dd, dq
+
+
+def key_window_backward(q, k, v, do, lse, dd, cu_seqlens, causal: bool, scale: float,
+                        kv_head: int, c_lo: int, c_hi: int, row_block: int = 512):
+    """dK_j and dV_j of key/value head `kv_head` for the keys c_lo <= j < c_hi
+    of one segment, summed over the query heads of its group, from the row
+    statistics LSE [Hq, T] (natural log) and D [Hq, T] of the rows that see
+    them (e.g. from head_rows over those rows; other entries are not read).
+    With P_ij = exp(S_ij - LSE_i) and dS_ij = P_ij (<dO_i, V_j> - D_i):
+    dK_j = scale sum_i dS_ij Q_i, dV_j = sum_i P_ij dO_i over the rows i that
+    see key j (i >= j within the segment when causal, every row otherwise).
+    Returns (dk [c_hi - c_lo, d], dv [c_hi - c_lo, d])."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    si = int(_segment_of(cu, np.array([c_lo]))[0])
+    a, b = int(cu[si]), int(cu[si + 1])
+    assert a <= c_lo < c_hi <= b, "the key window must lie inside one segment"
+    Hq, Hkv = _nheads(q), _nheads(k)
+    g = Hq // Hkv
+    kw = _head(k, kv_head)[c_lo:c_hi]
+    vw = _head(v, kv_head)[c_lo:c_hi]
+    dk = np.zeros_like(kw)
+    dv = np.zeros_like(vw)
+    cols = np.arange(c_lo, c_hi)[None, :]
+    for h in range(kv_head * g, (kv_head + 1) * g):
+        qh, doh = _head(q, h), _head(do, h)
+        for r0 in range(c_lo if causal else a, b, row_block):
+            r1 = min(b, r0 + row_block)
+            s = scale * (qh[r0:r1] @ kw.T)
+            if causal:
+                s = np.where(cols <= np.arange(r0, r1)[:, None], s, -np.inf)
+            p = np.exp(s - lse[h, r0:r1, None])
+            dor = doh[r0:r1]
+            ds = p * (dor @ vw.T - dd[h, r0:r1, None])
+            dk += scale * (ds.T @ qh[r0:r1])
+            dv += p.T @ dor
+    return dk, dv
+
+
 def _nheads(x) -> int:
     if hasattr(x, "num_heads"):
         return x.num_heads

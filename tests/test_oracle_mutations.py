@@ -10,6 +10,7 @@ import types
 import pytest
 
 import tests.test_oracle as pins
+import tests.test_oracle_stats as stat_pins
 
 SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                    "oracle", "attention.py")
@@ -30,6 +31,21 @@ MUTATIONS = {
     "segment_leak": ("kk = k[a:a + n, hk]\n                vv = v[a:a + n, hk]\n                s = _logits(q[r0:r1, h], kk, a, r0, causal, scale)\n                l, p",
                      "kk = k[max(0, a - 1):max(0, a - 1) + n, hk]\n                vv = v[max(0, a - 1):max(0, a - 1) + n, hk]\n                s = _logits(q[r0:r1, h], kk, a, r0, causal, scale)\n                l, p"),
     "visible_short": ("return (r1 - a) if causal else (b - a)", "return (r1 - a - 1) if causal else (b - a)"),
+    # the row-statistics pass and the key-window gradient
+    "rows_dq_no_scale": ("dd[sl], dq[sl] = orow, l, D, scale * (ds @ kk)",
+                         "dd[sl], dq[sl] = orow, l, D, (ds @ kk)"),
+    "rows_d_from_dq": ("D = np.sum(dor * orow, axis=1)\n            ds = p * (dor @ vv.T - D[:, None])\n            sl",
+                       "D = np.sum(dor * dor, axis=1)\n            ds = p * (dor @ vv.T - D[:, None])\n            sl"),
+    "rows_block_overrun": ("r1 = min(b, r_hi, r0 + row_block)", "r1 = min(b, r0 + row_block)"),
+    "window_mask_strict": ("s = np.where(cols <= np.arange(r0, r1)[:, None], s, -np.inf)",
+                           "s = np.where(cols < np.arange(r0, r1)[:, None], s, -np.inf)"),
+    "window_skips_diagonal_row": ("for r0 in range(c_lo if causal else a, b, row_block):",
+                                  "for r0 in range(c_lo + 1 if causal else a, b, row_block):"),
+    "window_no_d": ("ds = p * (dor @ vw.T - dd[h, r0:r1, None])", "ds = p * (dor @ vw.T)"),
+    "window_lse_log2": ("p = np.exp(s - lse[h, r0:r1, None])",
+                        "p = np.exp2(s - lse[h, r0:r1, None])"),
+    "window_one_head": ("for h in range(kv_head * g, (kv_head + 1) * g):",
+                        "for h in range(kv_head * g, kv_head * g + 1):"),
 }
 
 PIN_TESTS = [
@@ -43,6 +59,12 @@ PIN_TESTS = [
     ("test_gradient_finite_differences", [(True,), (False,)]),
     ("test_gqa_equals_repeated_mha", [()]),
     ("test_global_invariants", [()]),
+]
+
+# pins of the row-statistics pass and the key-window gradient
+STAT_PIN_TESTS = [
+    ("test_head_rows_match_torch", list(stat_pins.CASES)),
+    ("test_key_windows_from_row_stats_match_torch", list(stat_pins.CASES)),
 ]
 
 
@@ -59,11 +81,13 @@ def _mutant(name):
 def test_mutation_is_caught(name, monkeypatch):
     mutant = _mutant(name)
     monkeypatch.setattr(pins, "ora", mutant)
-    for test_name, cases in PIN_TESTS:
-        fn = getattr(pins, test_name)
-        for args in cases:
-            try:
-                fn(*args)
-            except Exception:
-                return  # detected
+    monkeypatch.setattr(stat_pins, "ora", mutant)
+    for module, tests in ((pins, PIN_TESTS), (stat_pins, STAT_PIN_TESTS)):
+        for test_name, cases in tests:
+            fn = getattr(module, test_name)
+            for args in cases:
+                try:
+                    fn(*args)
+                except Exception:
+                    return  # detected
     pytest.fail(f"planted mistake '{name}' passed every pin")
