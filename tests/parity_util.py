@@ -140,3 +140,56 @@ def gpu_invariants(o, lse, dq, dk, dv, q, k, v, do, cu_list, scale, causal=True)
     for name, r in worst.items():
         assert r < 5e-3, f"invariant {name} residual {r:.3e}"
     return worst
+
+
+class ErrAcc:
+    """Running max |err|, ||err||^2 and ||ref||^2 of one tensor compared in
+    pieces (per head, per row range), checked against the same per-tensor
+    tolerance as check_close once every piece is in."""
+
+    def __init__(self, name: str):
+        self.name = name
+        self.max_abs = 0.0
+        self.sq_err = 0.0
+        self.sq_ref = 0.0
+        self.n = 0
+
+    def add(self, got, ref):
+        got = np.asarray(got, dtype=np.float64)
+        ref = np.asarray(ref, dtype=np.float64)
+        assert got.shape == ref.shape, f"{self.name}: shape {got.shape} vs {ref.shape}"
+        assert np.all(np.isfinite(got)), f"{self.name}: non-finite values in device output"
+        diff = got - ref
+        if diff.size:
+            self.max_abs = max(self.max_abs, float(np.max(np.abs(diff))))
+        self.sq_err += float(np.sum(diff * diff))
+        self.sq_ref += float(np.sum(ref * ref))
+        self.n += diff.size
+
+    def check(self, max_abs: float = MAX_ABS, rel_l2: float = REL_L2):
+        rel = math.sqrt(self.sq_err / self.sq_ref) if self.sq_ref > 0 else math.sqrt(self.sq_err)
+        log(f"    {self.name:5s} max|err| {self.max_abs:.3e}  relL2 {rel:.3e}  (n={self.n})"
+            f"  margins {max_abs / max(self.max_abs, 1e-30):.1f}x / {rel_l2 / max(rel, 1e-30):.1f}x")
+        assert self.max_abs <= max_abs, f"{self.name}: max abs error {self.max_abs:.3e} > {max_abs}"
+        assert rel <= rel_l2, f"{self.name}: relative L2 error {rel:.3e} > {rel_l2}"
+        return self.max_abs, rel
+
+
+def host_workers() -> int:
+    """Threads for running independent oracle pieces side by side (the
+    oracle's elementwise numpy work is single-threaded per call): the
+    process's CPUs, at most 16."""
+    import os
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def run_pieces(fn, pieces):
+    """fn(piece) for every piece on host_workers() threads, each call with a
+    single-threaded BLAS (numpy releases the GIL inside its array work).
+    Returns the results in the order of `pieces`."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1):
+        with ThreadPoolExecutor(max_workers=host_workers()) as ex:
+            return list(ex.map(fn, pieces))

@@ -261,17 +261,32 @@ def test_single_638976_h4():
                     per_seg_random=48, tail_cols=96, max_rows=96)
 
 
-def test_stream_batches_gqa():
+def _stream_cases():
+    """Batches of the lognormal GQA stream checked against the oracle: every
+    single-sequence batch but the longest (which has a test of its own), the
+    most- and least-segmented packed batches, the packed batches with the
+    longest and the shortest longest segment, and two more spread over the
+    stream."""
     stream = wl.stream_config5()
-    # the most-segmented packed batch and the shortest single-sequence batch
-    packed = max(range(len(stream)), key=lambda i: stream[i].num_seqs)
-    single = min((i for i in range(len(stream)) if stream[i].num_seqs == 1),
-                 key=lambda i: stream[i].max_seqlen)
-    for i in (packed, single):
-        w = stream[i]
-        _sampled_parity(w, device_gen=True, heads=[0, 17, 31], kv_heads=[0, 7],
-                        per_seg_random=4 if w.num_seqs > 1 else 32, tail_cols=64,
-                        max_rows=64)
+    idx = range(len(stream))
+    singles = [i for i in idx if stream[i].num_seqs == 1]
+    longest = max(singles, key=lambda i: stream[i].max_seqlen)
+    packed = [i for i in idx if stream[i].num_seqs > 1]
+    picks = {max(packed, key=lambda i: stream[i].num_seqs),
+             min(packed, key=lambda i: stream[i].num_seqs),
+             max(packed, key=lambda i: stream[i].max_seqlen),
+             min(packed, key=lambda i: stream[i].max_seqlen),
+             packed[0], packed[len(packed) // 3], packed[2 * len(packed) // 3]}
+    return sorted(set(singles) - {longest}) + sorted(picks)
+
+
+@pytest.mark.parametrize("batch", _stream_cases())
+def test_stream_batches_gqa(batch):
+    w = wl.stream_config5()[batch]
+    _sampled_parity(w, device_gen=True, heads=[0, 17, 31], kv_heads=[0, 7],
+                    per_seg_random=4 if w.num_seqs > 1 else 32, tail_cols=64,
+                    tail_segs=sorted({0, int(np.argmax(w.lengths)), w.num_seqs - 1}),
+                    max_rows=64)
 
 
 def test_stream_longest_batch_gqa():
