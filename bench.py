@@ -27,6 +27,18 @@ WORKLOADS = {
 
 METRIC = "causal attn fwd+bwd TFLOP/s and % bf16 MFMA peak vs seq length (1 GPU)"
 
+# the sequence-length sweep timed in the same run as the main line: single
+# sequences over 4 heads (one GPU's share of a 32-head layer over 8 GPUs)
+# from 4K to the 638,976-token ("624K") length, and the packed 65,536-token
+# batch over 32 heads; (label, lengths, heads, steps, warmup)
+SWEEP = [
+    ("single4096_h4_d128", [4096], 4, 20, 3),
+    ("single16384_h4_d128", [16384], 4, 10, 3),
+    ("single131072_h4_d128", [131072], 4, 5, 2),
+    ("single638976_h4_d128", [638976], 4, 3, 1),
+    ("packed65536_loguniform128-8192_h32_d128", None, 32, 10, 3),
+]
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__)
@@ -35,6 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="single131072")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the sequence-length sweep timed after the main line")
     ap.add_argument("--cpu-sample-tokens", type=int, default=12288,
                     help="causal prefix length the CPU oracle is timed on")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -56,9 +70,22 @@ def copy_calibration(mib: int):
     print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or the machine type."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(w, inputs, sample_tokens: int):
     """Time the fp64 oracle (as it stands) on the causal prefix of head 0:
-    its full forward + backward over the first `sample_tokens` tokens."""
+    its full forward + backward over the first `sample_tokens` tokens.  The
+    full workload's oracle time is extrapolated from the measured rate."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -75,16 +102,22 @@ def cpu_baseline(w, inputs, sample_tokens: int):
     ora.backward(q, k, v, do, cu, w.causal, w.softmax_scale)
     dt = time.perf_counter() - t0
     flops = acc.fwd_bwd_flops([S], 1, w.head_dim, w.causal)
+    full = acc.fwd_bwd_flops(w.lengths, w.heads_q, w.head_dim, w.causal)
+    rate = flops / dt
     threads = max([p.get("num_threads", 1) for p in threadpool_info()
                    if p.get("user_api") == "blas"] or [1])
     return {
-        "value": flops / dt / 1e12,
+        "value": rate / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
+        "cpu_model": cpu_model(),
         "sample": (f"fp64 forward+backward of the causal prefix of the first {S} tokens of "
                    f"query head 0 of the {w.name} workload ({flops:.3e} counted FLOPs in "
-                   f"{dt:.2f} s; host {platform.processor() or platform.machine()})"),
+                   f"{dt:.2f} s)"),
+        "full_workload_s_extrapolated": round(full / rate, 1),
+        "extrapolation": (f"{full:.3e} counted FLOPs of one full step at the sample's "
+                          f"measured rate (extrapolated, not run)"),
     }
 
 
@@ -105,6 +138,80 @@ def recorded_traffic(workload_name: str, kernel: str):
     if "fetch_bytes" not in k or "write_bytes" not in k:
         return None
     return k["fetch_bytes"] + k["write_bytes"]
+
+
+def time_steps(w, steps: int, warmup: int):
+    """Mean wall time (ms) of `steps` fwd+bwd steps of workload w with inputs
+    resident in HBM, after `warmup` untimed steps; the library's per-kernel
+    times (HIP events on the launch streams) come with it."""
+    import torch
+
+    from paper_2511_13198_amd import pdyattn
+    from paper_2511_13198_amd import workloads as wl
+    T, hq, hkv, d = w.total_tokens, w.heads_q, w.heads_kv, w.head_dim
+    dev = torch.device("cuda:0")
+    inputs = wl.device_inputs(T, hq, hkv, d, device="cuda")
+    q, k, v, do = inputs["q"], inputs["k"], inputs["v"], inputs["do"]
+    cu = torch.from_numpy(w.cu_seqlens()).to(dev)
+    maxlen, scale, causal = w.max_seqlen, w.softmax_scale, w.causal
+    o = torch.empty_like(q)
+    lse = torch.empty((hq, T), dtype=torch.float32, device=dev)
+    dq = torch.empty((T, hq, d), dtype=torch.float32, device=dev)
+    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=dev)
+    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=dev)
+    n = w.num_seqs
+    wsf = torch.empty(max(256, pdyattn.fwd_workspace_size(T, n, maxlen, hq, hkv, d)),
+                      dtype=torch.uint8, device=dev)
+    wsb = torch.empty(max(256, pdyattn.bwd_workspace_size(T, n, maxlen, hq, hkv, d)),
+                      dtype=torch.uint8, device=dev)
+
+    def step():
+        pdyattn.attn_fwd(q, k, v, cu, maxlen, causal, scale, out=o, lse=lse, workspace=wsf)
+        pdyattn.attn_bwd(q, k, v, o, lse, do, cu, maxlen, causal, scale, dq=dq, dk=dk, dv=dv,
+                         workspace=wsb)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    pdyattn.profile_start()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = pdyattn.profile_stop()
+    kernels_ms = {name: tot / cnt for name, (cnt, tot) in prof.items()}
+    return (t1 - t0) / steps * 1e3, kernels_ms, inputs
+
+
+def sweep(main_name: str, main_ms: float, main_kms: dict, main_steps: int, main_warmup: int):
+    """The sweep lines: fwd+bwd TFLOP/s and % of peak per length (the main
+    workload's line is the main measurement itself)."""
+    import torch
+
+    from paper_2511_13198_amd import accounting as acc
+    from paper_2511_13198_amd import workloads as wl
+    out = []
+    for label, lengths, heads, steps, warmup in SWEEP:
+        w = wl.config(2) if lengths is None else wl.Workload(label, lengths, heads, heads, 128)
+        if w.name == main_name:
+            ms, kms, steps, warmup = main_ms, main_kms, main_steps, main_warmup
+        else:
+            ms, kms, inputs = time_steps(w, steps, warmup)
+            del inputs
+            torch.cuda.empty_cache()
+        flops = acc.fwd_bwd_flops(w.lengths, w.heads_q, w.head_dim, w.causal)
+        tf = flops / (ms / 1e3) / 1e12
+        out.append({"workload": w.name, "tokens": w.total_tokens, "segments": w.num_seqs,
+                    "max_seqlen": w.max_seqlen, "heads_q": w.heads_q, "heads_kv": w.heads_kv,
+                    "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 4),
+                    "tflops": round(tf, 2),
+                    "pct_of_peak": round(100.0 * tf / acc.PEAK_BF16_TFLOPS, 2),
+                    "kernels_ms": {kk: round(vv, 4) for kk, vv in kms.items()}})
+        print(f"[bench] sweep {w.name}: {ms:.3f} ms/step, {tf:.1f} TFLOP/s", file=sys.stderr,
+              flush=True)
+    return out
 
 
 def main():
@@ -133,44 +240,13 @@ def main():
 
     w = wl.config(WORKLOADS[args.workload])
     T, hq, hkv, d = w.total_tokens, w.heads_q, w.heads_kv, w.head_dim
-    dev = torch.device("cuda:0")
-    inputs = wl.device_inputs(T, hq, hkv, d, device="cuda")
-    q, k, v, do = inputs["q"], inputs["k"], inputs["v"], inputs["do"]
-    cu = torch.from_numpy(w.cu_seqlens()).to(dev)
-    maxlen, scale, causal = w.max_seqlen, w.softmax_scale, w.causal
-    o = torch.empty_like(q)
-    lse = torch.empty((hq, T), dtype=torch.float32, device=dev)
-    dq = torch.empty((T, hq, d), dtype=torch.float32, device=dev)
-    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=dev)
-    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=dev)
-    n = w.num_seqs
-    wsf = torch.empty(max(256, pdyattn.fwd_workspace_size(T, n, maxlen, hq, hkv, d)),
-                      dtype=torch.uint8, device=dev)
-    wsb = torch.empty(max(256, pdyattn.bwd_workspace_size(T, n, maxlen, hq, hkv, d)),
-                      dtype=torch.uint8, device=dev)
-
-    def step():
-        pdyattn.attn_fwd(q, k, v, cu, maxlen, causal, scale, out=o, lse=lse, workspace=wsf)
-        pdyattn.attn_bwd(q, k, v, o, lse, do, cu, maxlen, causal, scale, dq=dq, dk=dk, dv=dv,
-                         workspace=wsb)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    print(f"[bench] {w.name}: warmup done, timing {args.steps} steps", file=sys.stderr, flush=True)
-    pdyattn.profile_start()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    prof = pdyattn.profile_stop()
-    ms = (t1 - t0) / args.steps * 1e3
+    n, maxlen, causal = w.num_seqs, w.max_seqlen, w.causal
+    print(f"[bench] {w.name}: {args.warmup} warmup + {args.steps} timed steps", file=sys.stderr,
+          flush=True)
+    ms, kernels_ms, inputs = time_steps(w, args.steps, args.warmup)
     flops = acc.fwd_bwd_flops(w.lengths, hq, d, causal)
     value = flops / (ms / 1e3) / 1e12
 
-    kernels_ms = {name: tot / cnt for name, (cnt, tot) in prof.items()}
     dom = max((kname for kname in kernels_ms if kname in acc.KERNEL_PRODUCTS),
               key=lambda kname: kernels_ms[kname])
     dom_flops = acc.kernel_flops(dom, w.lengths, hq, d, causal)
@@ -187,6 +263,16 @@ def main():
     print(f"[bench] {ms:.3f} ms/step, {value:.1f} TFLOP/s; kernels (avg ms): "
           + ", ".join(f"{kk}={vv:.3f}" for kk, vv in kernels_ms.items()),
           file=sys.stderr, flush=True)
+
+    per_kernel = {kname: {"algorithmic_tflops": round(acc.kernel_flops(kname, w.lengths, hq, d, causal)
+                                                      / (kms / 1e3) / 1e12, 2),
+                          "issued_tflops": round(acc.kernel_issued_flops(kname, w.lengths, hq, d,
+                                                                         causal)
+                                                 / (kms / 1e3) / 1e12, 2)}
+                  for kname, kms in kernels_ms.items() if kname in acc.KERNEL_PRODUCTS}
+    lengths = None
+    if not args.no_sweep:
+        lengths = sweep(w.name, ms, kernels_ms, args.steps, args.warmup)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -219,8 +305,10 @@ def main():
         },
         "pct_of_peak": round(100.0 * value / acc.PEAK_BF16_TFLOPS, 2),
         "kernels_ms": {kk: round(vv, 4) for kk, vv in kernels_ms.items()},
+        "kernels_tflops": per_kernel,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "vs_seq_length": lengths,
     }
     print(json.dumps(out), flush=True)
 
