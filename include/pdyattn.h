@@ -162,6 +162,30 @@ pdy_status attn_validate_cu_seqlens(const int32_t* cu_seqlens, int32_t num_seqs,
                                     int32_t total_tokens, int32_t* max_seqlen_out,
                                     void* stream);
 
+/* attn_bwd for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same computation, arguments and outputs as attn_bwd, without the
+ * workspace.  Its scratch (the tile schedules, D and any split-K partial
+ * gradients) is a static device array of 64 MiB per GPU, held from the
+ * first call on that GPU until the process ends.  Sizes whose schedules and
+ * D alone exceed 64 MiB (Hq * T beyond about 16.7 million (row, head)
+ * pairs) return PDY_ERR_WORKSPACE before anything is launched.  A launch
+ * small enough to split (see above) whose partial gradients would not fit
+ * takes fewer parts; its results may then differ from attn_bwd's in
+ * rounding (well inside the stated tolerance), otherwise they equal
+ * attn_bwd's bit for bit.  The call allocates nothing (no hipMalloc, no
+ * library allocation); on its first use on a device it looks up that
+ * device's address of the array.  The array keeps the last call's contents,
+ * none of which a call reads before writing it.  Every call on one GPU uses
+ * the same array: calls that overlap on one GPU (other streams, other
+ * threads) race and must be serialised by the caller. */
+pdy_status attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
+                            const float* lse, const void* dout, const int32_t* cu_seqlens,
+                            int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen,
+                            int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                            int32_t causal, float scale, float* dq, float* dk, float* dv,
+                            void* stream);
+
 /* Static text for a status code. */
 const char* pdy_status_string(int32_t status);
 

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "bwd.hpp"
@@ -243,6 +244,12 @@ size_t bwd_split_bytes(const Sizes& sq, const Sizes& sk) {
   return (pk > 1 ? 2 * part_kv_bytes(sk, pk) : 0) + (pq > 1 ? part_o_bytes(sq, pq) : 0);
 }
 
+// workspace of a (non-chunk) backward: both tile schedules, D and any split-K partials
+size_t bwd_workspace_bytes(const Sizes& s) {
+  return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
+         bwd_split_bytes(s, s);
+}
+
 // A single segment (N = 1: by the contract cu = [0, T], and max_seqlen = T)
 // needs no schedule: item i is its level nt - 1 - i, so no plan is built.
 bool needs_plan(const Sizes& s) { return s.N > 1; }
@@ -366,8 +373,7 @@ size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
-         bwd_split_bytes(s, s);
+  return bwd_workspace_bytes(s);
 }
 
 }  // extern "C"
@@ -467,14 +473,27 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
                     const void* dout, const int32_t* cu, const Sizes& s, const Sizes& sk,
                     int32_t causal, float scale, float* dq, float* dk, float* dv,
                     void* workspace, size_t workspace_bytes, void* stream, const Chunk& c,
-                    const char* who) {
+                    const char* who, bool fit_splits = false) {
   pdy_status st;
   const int nwq = fwd_waves(s);
   const int qtile = 32 * nwq;
   // (no split-K for a context-parallel pair, as in the forward)
-  const int nsplit_kv = c.on || sk.T == 0 ? 1 : dkdv_split(s, sk);
-  const int nsplit_q = c.on ? 1 : dq_split(s, sk);
-  const size_t need = bwd_need(s, sk) + (c.on ? 0 : bwd_split_bytes(s, sk));
+  int nsplit_kv = c.on || sk.T == 0 ? 1 : dkdv_split(s, sk);
+  int nsplit_q = c.on ? 1 : dq_split(s, sk);
+  auto need_for = [&](int pk, int pq) {
+    return bwd_need(s, sk) + (pk > 1 ? 2 * part_kv_bytes(sk, pk) : 0) +
+           (pq > 1 ? part_o_bytes(s, pq) : 0);
+  };
+  // fit_splits: a fixed-size workspace takes fewer split-K parts (the larger
+  // partial buffer halved first) when the chosen ones do not fit
+  while (fit_splits && need_for(nsplit_kv, nsplit_q) > workspace_bytes &&
+         (nsplit_kv > 1 || nsplit_q > 1)) {
+    const size_t bk = nsplit_kv > 1 ? 2 * part_kv_bytes(sk, nsplit_kv) : 0;
+    const size_t bq = nsplit_q > 1 ? part_o_bytes(s, nsplit_q) : 0;
+    if (bq >= bk) nsplit_q = nsplit_q == 2 ? 1 : nsplit_q / 2;
+    else nsplit_kv = nsplit_kv == 2 ? 1 : nsplit_kv / 2;
+  }
+  const size_t need = need_for(nsplit_kv, nsplit_q);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -591,6 +610,68 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   return PDY_OK;
 }
 
+// Argument checks of attn_bwd and attn_bwd_noalloc (everything but the
+// workspace); s is filled in.  T = 0 passes with PDY_OK before the pointers
+// are looked at.
+pdy_status bwd_checks(const void* q, const void* k, const void* v, const void* o,
+                      const float* lse, const void* dout, const int32_t* cu_seqlens,
+                      int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen,
+                      int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                      int32_t causal, float scale, float* dq, float* dk, float* dv, Sizes* s) {
+  pdy_status st;
+  if ((st = check_sizes(total_tokens, num_seqs, max_seqlen, num_heads_q, num_heads_kv, head_dim,
+                        s)) != PDY_OK)
+    return st;
+  if ((st = check_scale(scale, causal)) != PDY_OK) return st;
+  if (s->T == 0) return PDY_OK;
+  if ((st = check_ptr(q, "q")) || (st = check_ptr(k, "k")) || (st = check_ptr(v, "v")) ||
+      (st = check_ptr(o, "o")) || (st = check_ptr(lse, "lse")) ||
+      (st = check_ptr(dout, "dout")) || (st = check_ptr(dq, "dq")) ||
+      (st = check_ptr(dk, "dk")) || (st = check_ptr(dv, "dv")))
+    return st;
+  if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
+    return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
+  return PDY_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch of attn_bwd_noalloc, for callers that cannot allocate.  A
+// file-scope device array: every GPU the library runs on holds its own copy
+// (kScratchBytes) from the first use until the process ends.  In host code
+// `scratch` only names the symbol; its device address on the current device
+// comes from hipGetSymbolAddress, looked up once per device and kept.
+// Nothing in it has to start at zero: each call writes every scratch entry
+// it reads (schedules, D, partial gradients) before reading it.  Calls that
+// overlap on one GPU share the array and race.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch.
+pdy_status scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(PDY_ERR_UNSUPPORTED, "device %d is beyond the %d the scratch table covers", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr) return fail(PDY_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PDY_OK;
+}
+
 // sizes of a chunk: one segment of t tokens
 pdy_status chunk_sizes(int32_t tq, int32_t tk, int32_t hq, int32_t hkv, int32_t d, Sizes* sq,
                        Sizes* sk) {
@@ -673,22 +754,42 @@ pdy_status attn_bwd(const void* q, const void* k, const void* v, const void* o, 
   g_err[0] = 0;
   Sizes s;
   pdy_status st;
-  if ((st = check_sizes(total_tokens, num_seqs, max_seqlen, num_heads_q, num_heads_kv, head_dim,
-                        &s)) != PDY_OK)
+  if ((st = bwd_checks(q, k, v, o, lse, dout, cu_seqlens, num_seqs, total_tokens, max_seqlen,
+                       num_heads_q, num_heads_kv, head_dim, causal, scale, dq, dk, dv, &s)) !=
+          PDY_OK ||
+      s.T == 0)
     return st;
-  if ((st = check_scale(scale, causal)) != PDY_OK) return st;
-  if (s.T == 0) return PDY_OK;
-  if ((st = check_ptr(q, "q")) || (st = check_ptr(k, "k")) || (st = check_ptr(v, "v")) ||
-      (st = check_ptr(o, "o")) || (st = check_ptr(lse, "lse")) ||
-      (st = check_ptr(dout, "dout")) || (st = check_ptr(dq, "dq")) ||
-      (st = check_ptr(dk, "dk")) || (st = check_ptr(dv, "dv")) ||
-      (st = check_ptr(workspace, "workspace")))
-    return st;
-  if (cu_seqlens == nullptr) return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is NULL");
-  if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3u) != 0)
-    return fail(PDY_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
+  if ((st = check_ptr(workspace, "workspace")) != PDY_OK) return st;
   return bwd_impl(q, k, v, o, lse, dout, cu_seqlens, s, s, causal, scale, dq, dk, dv, workspace,
                   workspace_bytes, stream, Chunk{}, "attn_bwd");
+}
+
+pdy_status attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
+                            const float* lse, const void* dout, const int32_t* cu_seqlens,
+                            int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen,
+                            int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim,
+                            int32_t causal, float scale, float* dq, float* dk, float* dv,
+                            void* stream) {
+  g_err[0] = 0;
+  Sizes s;
+  pdy_status st;
+  if ((st = bwd_checks(q, k, v, o, lse, dout, cu_seqlens, num_seqs, total_tokens, max_seqlen,
+                       num_heads_q, num_heads_kv, head_dim, causal, scale, dq, dk, dv, &s)) !=
+          PDY_OK ||
+      s.T == 0)
+    return st;
+  // the scratch attn_bwd takes from its workspace: the tile schedules and D,
+  // plus split-K partial gradients where those fit (else fewer parts)
+  const size_t need = bwd_need(s, s);
+  if (need > kScratchBytes)
+    return fail(PDY_ERR_WORKSPACE,
+                "attn_bwd_noalloc needs %zu bytes of scratch for these sizes, more than its "
+                "static scratch of %zu bytes (call attn_bwd with a workspace instead)",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_ptr(&ws)) != PDY_OK) return st;
+  return bwd_impl(q, k, v, o, lse, dout, cu_seqlens, s, s, causal, scale, dq, dk, dv, ws,
+                  kScratchBytes, stream, Chunk{}, "attn_bwd_noalloc", /*fit_splits=*/true);
 }
 
 pdy_status attn_bwd_chunk(const void* q, const void* k, const void* v, const void* o,

@@ -25,7 +25,7 @@ PDY_ERR_HIP = -4
 SYMBOLS = ("attn_fwd_workspace_size", "attn_bwd_workspace_size", "attn_fwd", "attn_bwd",
            "attn_fwd_chunk_workspace_size", "attn_bwd_chunk_workspace_size", "attn_fwd_chunk",
            "attn_bwd_chunk", "attn_merge",
-           "attn_validate_cu_seqlens", "pdy_status_string", "pdy_last_error",
+           "attn_validate_cu_seqlens", "attn_bwd_noalloc", "pdy_status_string", "pdy_last_error",
            "pdy_kernel_count", "pdy_kernel_name", "pdy_profile_start", "pdy_profile_stop")
 
 
@@ -71,6 +71,9 @@ def lib() -> ctypes.CDLL:
     L.attn_merge.restype = i32
     L.attn_validate_cu_seqlens.argtypes = [vp, i32, i32, ctypes.POINTER(i32), vp]
     L.attn_validate_cu_seqlens.restype = i32
+    L.attn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
+                                   f32, vp, vp, vp, vp]
+    L.attn_bwd_noalloc.restype = i32
     L.pdy_status_string.argtypes = [i32]
     L.pdy_status_string.restype = ctypes.c_char_p
     L.pdy_last_error.argtypes = []
@@ -189,10 +192,9 @@ def attn_fwd(q, k, v, cu_seqlens, max_seqlen: Optional[int] = None, causal: bool
     return out, lse
 
 
-def attn_bwd(q, k, v, o, lse, dout, cu_seqlens, max_seqlen: Optional[int] = None,
-             causal: bool = True, scale: Optional[float] = None, dq=None, dk=None, dv=None,
-             workspace=None) -> Tuple:
-    """dQ [T, Hq, d], dK, dV [T, Hkv, d] (fp32) of sum(dout * O)."""
+def _bwd_args(q, k, v, o, lse, dout, cu_seqlens, max_seqlen, scale, dq, dk, dv):
+    """Checked shapes and outputs of a backward call (outputs allocated by
+    torch when not given)."""
     import torch
     for t, name in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
         _check_tensor(t, name, torch.bfloat16, 3)
@@ -208,22 +210,55 @@ def attn_bwd(q, k, v, o, lse, dout, cu_seqlens, max_seqlen: Optional[int] = None
         max_seqlen = validate_cu_seqlens(cu_seqlens, T)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
-    n = cu_seqlens.numel() - 1
     if dq is None:
         dq = torch.empty((T, hq, d), dtype=torch.float32, device=q.device)
     if dk is None:
         dk = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
     if dv is None:
         dv = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    for t, name, shape in ((dq, "dq", (T, hq, d)), (dk, "dk", (T, hkv, d)),
+                           (dv, "dv", (T, hkv, d))):
+        _check_tensor(t, name, torch.float32, 3)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} must be {list(shape)}")
+    n = cu_seqlens.numel() - 1
+    return T, hq, hkv, d, n, int(max_seqlen), float(scale), dq, dk, dv
+
+
+def attn_bwd(q, k, v, o, lse, dout, cu_seqlens, max_seqlen: Optional[int] = None,
+             causal: bool = True, scale: Optional[float] = None, dq=None, dk=None, dv=None,
+             workspace=None) -> Tuple:
+    """dQ [T, Hq, d], dK, dV [T, Hkv, d] (fp32) of sum(dout * O)."""
+    T, hq, hkv, d, n, max_seqlen, scale, dq, dk, dv = _bwd_args(
+        q, k, v, o, lse, dout, cu_seqlens, max_seqlen, scale, dq, dk, dv)
     need = bwd_workspace_size(T, n, max_seqlen, hq, hkv, d)
     if workspace is None:
         workspace = _ws(need, q.device)
     st = lib().attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                        dout.data_ptr(), cu_seqlens.data_ptr(), n, T, int(max_seqlen), hq, hkv, d,
-                        int(bool(causal)), float(scale), dq.data_ptr(), dk.data_ptr(),
+                        dout.data_ptr(), cu_seqlens.data_ptr(), n, T, max_seqlen, hq, hkv, d,
+                        int(bool(causal)), scale, dq.data_ptr(), dk.data_ptr(),
                         dv.data_ptr(), workspace.data_ptr(),
                         workspace.numel() * workspace.element_size(), _stream_handle(q.device))
     _check(st, "attn_bwd")
+    return dq, dk, dv
+
+
+def attn_bwd_noalloc(q, k, v, o, lse, dout, cu_seqlens, max_seqlen: Optional[int] = None,
+                     causal: bool = True, scale: Optional[float] = None, dq=None, dk=None,
+                     dv=None) -> Tuple:
+    """attn_bwd without a workspace: the library takes its scratch from a
+    static device array of fixed size (PdyError with PDY_ERR_WORKSPACE when
+    the sizes need more).  With dq, dk, dv given and max_seqlen known, this
+    call allocates nothing.  Calls that overlap on one GPU share that
+    scratch and must not run concurrently."""
+    T, hq, hkv, d, n, max_seqlen, scale, dq, dk, dv = _bwd_args(
+        q, k, v, o, lse, dout, cu_seqlens, max_seqlen, scale, dq, dk, dv)
+    st = lib().attn_bwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                lse.data_ptr(), dout.data_ptr(), cu_seqlens.data_ptr(), n, T,
+                                max_seqlen, hq, hkv, d, int(bool(causal)), scale,
+                                dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                _stream_handle(q.device))
+    _check(st, "attn_bwd_noalloc")
     return dq, dk, dv
 
 

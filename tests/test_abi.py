@@ -202,3 +202,30 @@ def test_chunk_noops_and_workspace_sizes():
     assert L.attn_merge(FAKE, FAKE, FAKE, FAKE, 10, 4, 96, FAKE, FAKE, None) == P.PDY_ERR_UNSUPPORTED
     assert L.attn_merge(FAKE, FAKE, FAKE, FAKE, 0, 4, 128, 0, 0, None) == P.PDY_OK
     assert L.attn_merge(FAKE, 0, FAKE, FAKE, 10, 4, 128, FAKE, FAKE, None) == P.PDY_ERR_INVALID_ARG
+
+
+def _bwd_noalloc(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, do=FAKE, cu=FAKE, n=1, T=512, maxlen=512,
+             hq=8, hkv=8, d=128, causal=1, scale=0.1, dq=FAKE, dk=FAKE, dv=FAKE, stream=None)
+    a.update(kw)
+    return P.lib().attn_bwd_noalloc(a["q"], a["k"], a["v"], a["o"], a["lse"], a["do"], a["cu"],
+                                    a["n"], a["T"], a["maxlen"], a["hq"], a["hkv"], a["d"],
+                                    a["causal"], a["scale"], a["dq"], a["dk"], a["dv"],
+                                    a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(dq=0), P.PDY_ERR_INVALID_ARG, "dq is NULL"),
+    (dict(maxlen=511), P.PDY_ERR_INVALID_ARG, "num_seqs = 1"),
+    (dict(d=80), P.PDY_ERR_UNSUPPORTED, "head_dim"),
+    # D alone (fp32 [Hq, T]) is 64 MiB here: beyond the static scratch
+    (dict(T=1 << 20, maxlen=1 << 20, hq=16, hkv=4), P.PDY_ERR_WORKSPACE, "static scratch"),
+])
+def test_bwd_noalloc_argument_errors(kw, status, msg):
+    st = _bwd_noalloc(**kw)
+    assert st == status, (st, P.last_error())
+    assert msg in P.last_error()
+
+
+def test_bwd_noalloc_empty_batch_is_noop():
+    assert _bwd_noalloc(T=0, maxlen=0, q=0, dq=0) == P.PDY_OK
