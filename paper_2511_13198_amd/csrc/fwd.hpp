@@ -89,6 +89,49 @@ struct FwdArgs {
 // key offset within a 32-key block held in accumulator register r (lane half 0)
 __device__ __forceinline__ constexpr int acc_row_off(int r) { return (r >> 2) * 8 + (r & 3); }
 
+// Epilogue of a forward workgroup's wave: normalise its 32 rows and write O
+// (bf16) and LSE (natural log), or, for a split-K part, the part's fp32 O and
+// LSE.  A row that saw no key (possible for a chunk or a part) gets O = 0 and
+// LSE = -inf.  m: the base-2 exponent offset; lsum: this lane's partial row
+// sum (the other half of the row's keys is on lane l ^ 32).
+template <int D>
+__device__ __forceinline__ void fwd_epilogue(const FwdArgs& a, const f32x16 (&oacc)[D / 32],
+                                             float m, float lsum, int row, int seg_hi, int h,
+                                             int part, int hh) {
+  const size_t qstride = (size_t)a.hq * D;
+  const float ltot = lsum + partner32(lsum);
+  if (row >= seg_hi) return;
+  const bool seen = ltot > 0.f;
+  const float inv = seen ? 1.f / ltot : 0.f;
+  const float lse = seen ? (m + __builtin_log2f(ltot)) * kLn2 : -INFINITY;
+  if (a.nsplit > 1) {
+    float* op = a.part_o + ((size_t)part * a.total_tokens + row) * qstride + (size_t)h * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 v = {oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv,
+                         oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv};
+        *reinterpret_cast<f32x4*>(op + db * 32 + g * 8 + hh * 4) = v;
+      }
+    if (hh == 0) a.part_lse[((size_t)part * a.hq + h) * a.total_tokens + row] = lse;
+  } else {
+    uint16_t* op = a.o + (size_t)row * qstride + (size_t)h * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x2 v01 = {oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv};
+        f32x2 v23 = {oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv};
+        bf16x2 b01 = __builtin_convertvector(v01, bf16x2);
+        bf16x2 b23 = __builtin_convertvector(v23, bf16x2);
+        u32x2 pk = {__builtin_bit_cast(uint32_t, b01), __builtin_bit_cast(uint32_t, b23)};
+        *reinterpret_cast<u32x2*>(op + db * 32 + g * 8 + hh * 4) = pk;
+      }
+    if (hh == 0) a.lse[(size_t)h * a.total_tokens + row] = lse;
+  }
+}
+
 template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a) {
   using C = FwdCfg<D, NW>;
@@ -331,43 +374,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
     }
   }
 
-  // epilogue: normalise, write O (bf16) and LSE (natural log)
-  const float ltot = lsum + partner32(lsum);
-  if (row < seg_hi && a.nsplit > 1) {
-    // a part's O in fp32 and its LSE (a part that saw no key: O = 0, LSE = -inf)
-    const bool seen = ltot > 0.f;
-    const float inv = seen ? 1.f / ltot : 0.f;
-    float* op = a.part_o + ((size_t)part * a.total_tokens + row) * qstride + (size_t)h * D;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 v = {oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv,
-                         oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv};
-        *reinterpret_cast<f32x4*>(op + db * 32 + g * 8 + hh * 4) = v;
-      }
-    if (hh == 0)
-      a.part_lse[((size_t)part * a.hq + h) * a.total_tokens + row] =
-          seen ? (m + __builtin_log2f(ltot)) * kLn2 : -INFINITY;
-  } else if (row < seg_hi) {
-    // a row that saw no key (possible for a chunk) gets O = 0, LSE = -inf
-    const bool seen = ltot > 0.f;
-    const float inv = seen ? 1.f / ltot : 0.f;
-    uint16_t* op = a.o + (size_t)row * qstride + (size_t)h * D;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        f32x2 v01 = {oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv};
-        f32x2 v23 = {oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv};
-        bf16x2 b01 = __builtin_convertvector(v01, bf16x2);
-        bf16x2 b23 = __builtin_convertvector(v23, bf16x2);
-        u32x2 pk = {__builtin_bit_cast(uint32_t, b01), __builtin_bit_cast(uint32_t, b23)};
-        *reinterpret_cast<u32x2*>(op + db * 32 + g * 8 + hh * 4) = pk;
-      }
-    if (hh == 0)
-      a.lse[(size_t)h * a.total_tokens + row] = seen ? (m + __builtin_log2f(ltot)) * kLn2 : -INFINITY;
-  }
+  fwd_epilogue<D>(a, oacc, m, lsum, row, seg_hi, h, part, hh);
 }
 
 // n floats set to zero, 4 per thread
