@@ -32,8 +32,8 @@ METRIC = "causal attn fwd+bwd TFLOP/s and % bf16 MFMA peak vs seq length (1 GPU)
 # from 4K to the 638,976-token ("624K") length, and the packed 65,536-token
 # batch over 32 heads; (label, lengths, heads, steps, warmup)
 SWEEP = [
-    ("single4096_h4_d128", [4096], 4, 20, 3),
-    ("single16384_h4_d128", [16384], 4, 10, 3),
+    ("single4096_h4_d128", [4096], 4, 50, 5),
+    ("single16384_h4_d128", [16384], 4, 20, 3),
     ("single131072_h4_d128", [131072], 4, 5, 2),
     ("single638976_h4_d128", [638976], 4, 3, 1),
     ("packed65536_loguniform128-8192_h32_d128", None, 32, 10, 3),
@@ -140,10 +140,13 @@ def recorded_traffic(workload_name: str, kernel: str):
     return k["fetch_bytes"] + k["write_bytes"]
 
 
-def time_steps(w, steps: int, warmup: int):
+def time_steps(w, steps: int, warmup: int, events_in_timed: bool = True):
     """Mean wall time (ms) of `steps` fwd+bwd steps of workload w with inputs
-    resident in HBM, after `warmup` untimed steps; the library's per-kernel
-    times (HIP events on the launch streams) come with it."""
+    resident in HBM, after `warmup` untimed steps, and the library's
+    per-kernel times (HIP events recorded on each launch's stream): over the
+    timed steps themselves, or (events_in_timed=False, for sub-millisecond
+    steps where recording two events per launch would be part of what is
+    timed) over as many further steps after the timed ones."""
     import torch
 
     from paper_2511_13198_amd import pdyattn
@@ -173,13 +176,18 @@ def time_steps(w, steps: int, warmup: int):
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    pdyattn.profile_start()
+    if events_in_timed:
+        pdyattn.profile_start()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    if not events_in_timed:
+        pdyattn.profile_start()
+        for _ in range(steps):
+            step()
     prof = pdyattn.profile_stop()
     kernels_ms = {name: tot / cnt for name, (cnt, tot) in prof.items()}
     return (t1 - t0) / steps * 1e3, kernels_ms, inputs
@@ -198,7 +206,7 @@ def sweep(main_name: str, main_ms: float, main_kms: dict, main_steps: int, main_
         if w.name == main_name:
             ms, kms, steps, warmup = main_ms, main_kms, main_steps, main_warmup
         else:
-            ms, kms, inputs = time_steps(w, steps, warmup)
+            ms, kms, inputs = time_steps(w, steps, warmup, events_in_timed=False)
             del inputs
             torch.cuda.empty_cache()
         flops = acc.fwd_bwd_flops(w.lengths, w.heads_q, w.head_dim, w.causal)
