@@ -254,18 +254,23 @@ size_t bwd_workspace_bytes(const Sizes& s) {
 // needs no schedule: item i is its level nt - 1 - i, so no plan is built.
 bool needs_plan(const Sizes& s) { return s.N > 1; }
 
+// segment-major work order from this many tiles in the longest segment on
+constexpr int kSegMajorTiles = 8;
+
 pdy::Plan make_plan(int32_t* ws, const Sizes& s, int tile) {
   const int nt = tiles_of(s, tile);
   pdy::Plan p;
+  p.max_nt = nt;
+  p.seg_major = nt >= kSegMajorTiles;
   if (!needs_plan(s)) {
-    p.order = p.start = p.total = nullptr;
-    p.max_nt = nt;
+    p.order = p.start = p.total = p.cnt = p.before = nullptr;
     return p;
   }
   p.order = ws + s.N;
+  p.cnt = ws + 2 * s.N;
   p.start = ws + 2 * s.N + nt;
   p.total = ws + 2 * s.N + 2 * nt;
-  p.max_nt = nt;
+  p.before = ws + 2 * s.N + 2 * nt + 1;
   return p;
 }
 

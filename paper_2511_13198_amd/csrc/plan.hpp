@@ -2,13 +2,15 @@
 //
 // A packed batch (segments of arbitrary, skewed lengths) is cut into tiles of
 // BT tokens per segment.  Under a causal mask the cost of query tile j is
-// proportional to j + 1 (it visits tiles 0..j), so the work list is ordered by
-// descending tile level across all segments: every workgroup launched early
-// takes one of the longest remaining jobs (longest-processing-time-first),
-// which balances the tail of a launch when lengths are skewed.  The list is
-// never materialised: the plan stores the segments sorted by tile count and
-// the first item index of every level, and a kernel maps its item index to
-// (segment, level) with a binary search (plan_lookup in common.hpp).  The
+// proportional to j + 1 (it visits tiles 0..j).  The work list comes in two
+// orders (plan_lookup in common.hpp): by descending tile level across all
+// segments (every workgroup launched early takes one of the longest remaining
+// jobs, longest-processing-time-first), or segment by segment, longest
+// segment first and each segment's tiles heaviest first (neighbouring
+// workgroups then share the rows or keys they stream in L2).  The list is
+// never materialised: the plan stores the segments sorted by tile count, the
+// first item of every level and the first item of every tile-count group, and
+// a kernel maps its item index to (segment, level) with a binary search.  The
 // plan costs O(N + max_nt) per launch, also for batches of very many short
 // segments.
 #pragma once
@@ -21,9 +23,10 @@ constexpr int kPlanThreads = 1024;
 // tiles); larger ranges bin in the workspace
 constexpr int kLdsBuckets = 6144;
 
-// Workspace layout (int32): nt[N] | order[N] | cnt[max_nt] | start[max_nt] | total[1]
+// Workspace layout (int32):
+//   nt[N] | order[N] | cnt[max_nt] | start[max_nt] | total[1] | before[max_nt]
 __host__ __device__ inline size_t plan_ints(int n, int max_nt) {
-  return (size_t)2 * n + (size_t)2 * max_nt + 1;
+  return (size_t)2 * n + (size_t)3 * max_nt + 1;
 }
 
 // In-place suffix sum over a[0..n) by the whole workgroup: a[j] becomes
@@ -99,6 +102,7 @@ __device__ inline void build_plan(const int32_t* __restrict__ cu, int n, int bt,
   int32_t* cnt = order + n;
   int32_t* start = cnt + max_nt;
   int32_t* total = start + max_nt;
+  int32_t* before = total + 1;
   const int t = threadIdx.x;
   __shared__ int32_t wsum[kPlanThreads / 64 + 1];
   // per-count histogram and placement cursors: in LDS when they fit (many
@@ -142,10 +146,16 @@ __device__ inline void build_plan(const int32_t* __restrict__ cu, int n, int bt,
   }
   __syncthreads();
 
-  // 4. start[j] = sum_{j' > j} cnt[j'] (first item of level j); total items
-  for (int j = t; j < max_nt; j += kPlanThreads) start[j] = cnt[j];
+  // 4. start[j] = sum_{j' > j} cnt[j'] (first item of level j); total items;
+  // before[j] = tiles of the segments with more than j + 1 tiles (in the
+  // segment-major order the segments with exactly j + 1 tiles start there)
+  for (int j = t; j < max_nt; j += kPlanThreads) {
+    start[j] = cnt[j];
+    before[j] = (j + 1) * (cnt[j] - (j + 1 < max_nt ? cnt[j + 1] : 0));
+  }
   __syncthreads();
   const int items = suffix_sum(start, max_nt, false, wsum);
+  suffix_sum(before, max_nt, false, wsum);
   if (t == 0) *total = items;
 }
 
