@@ -193,3 +193,61 @@ def run_pieces(fn, pieces):
     with threadpool_limits(1):
         with ThreadPoolExecutor(max_workers=host_workers()) as ex:
             return list(ex.map(fn, pieces))
+
+
+def head_rows_and_key_windows(dev, outs, cu, causal, scale, h, windows, step=2048, sub=256):
+    """Every row of query head h (O, LSE, dQ) and dK, dV of its kv head on the
+    key windows [(lo, hi), ...] of a single segment cu = [0, T], against the
+    oracle's row statistics pass (head_rows) and key-window gradients
+    (key_window_backward), both run in pieces side by side on the host.
+    dev: device bf16 inputs q, k, v, do; outs: device outputs (o, lse, dq, dk,
+    dv)."""
+    import time
+
+    from oracle import attention as ora
+    o, lse, dq, dk, dv = outs
+    T, hq = dev["q"].shape[0], dev["q"].shape[1]
+    hkv = dev["k"].shape[1]
+    g = hq // hkv
+    hk = h // g
+    qs = dev["q"][:, hk * g:(hk + 1) * g].contiguous().cpu().double().numpy()
+    dos = dev["do"][:, hk * g:(hk + 1) * g].contiguous().cpu().double().numpy()
+    ks = dev["k"][:, hk:hk + 1].contiguous().cpu().double().numpy()
+    vs = dev["v"][:, hk:hk + 1].contiguous().cpu().double().numpy()
+    got_o = o[:, h].double().cpu().numpy()
+    got_l = lse[h].double().cpu().numpy()
+    got_q = dq[:, h].double().cpu().numpy()
+    got_k = dk[:, hk].double().cpu().numpy()
+    got_v = dv[:, hk].double().cpu().numpy()
+    pieces = [(hh, r0, min(T, r0 + step)) for hh in range(g) for r0 in range(0, T, step)]
+    t0 = time.perf_counter()
+    rows = run_pieces(lambda p: ora.head_rows(qs, ks, vs, dos, cu, causal, scale, p[0], p[1],
+                                              p[2]), pieces)
+    log(f"  oracle rows of {g} head(s): {len(pieces)} pieces in {time.perf_counter() - t0:.1f} s")
+    lse_all = np.zeros((g, T))
+    dd_all = np.zeros((g, T))
+    acc = {n: ErrAcc(n) for n in ("O", "LSE", "dQ")}
+    for (hh, r0, r1), (ro, rl, rd, rq) in zip(pieces, rows):
+        lse_all[hh, r0:r1] = rl
+        dd_all[hh, r0:r1] = rd
+        if hh == h - hk * g:
+            acc["O"].add(got_o[r0:r1], ro)
+            acc["LSE"].add(got_l[r0:r1], rl)
+            acc["dQ"].add(got_q[r0:r1], rq)
+    for a in acc.values():
+        a.check()
+    kpieces = [(c, min(hi, c + sub)) for lo, hi in windows for c in range(lo, hi, sub)]
+    t0 = time.perf_counter()
+    cols = run_pieces(lambda p: ora.key_window_backward(qs, ks, vs, dos, lse_all, dd_all, cu,
+                                                        causal, scale, 0, p[0], p[1]), kpieces)
+    log(f"  oracle key windows: {len(kpieces)} pieces in {time.perf_counter() - t0:.1f} s")
+    for lo, hi in windows:
+        acc = {n: ErrAcc(n) for n in ("dK", "dV")}
+        for (c0, c1), (rk, rv) in zip(kpieces, cols):
+            if lo <= c0 < hi:
+                acc["dK"].add(got_k[c0:c1], rk)
+                acc["dV"].add(got_v[c0:c1], rv)
+        log(f"   keys [{lo}, {hi}) of kv head {hk}: |dK| up to "
+            f"{float(np.max(np.abs(got_k[lo:hi]))):.3g}")
+        for a in acc.values():
+            a.check()
