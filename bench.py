@@ -30,13 +30,15 @@ METRIC = "causal attn fwd+bwd TFLOP/s and % bf16 MFMA peak vs seq length (1 GPU)
 # the sequence-length sweep timed in the same run as the main line: single
 # sequences over 4 heads (one GPU's share of a 32-head layer over 8 GPUs)
 # from 4K to the 638,976-token ("624K") length, and the packed 65,536-token
-# batch over 32 heads; (label, lengths, heads, steps, warmup)
+# batch over 32 heads; (label, lengths, heads, steps, warmup, events in the
+# timed steps: off for sub-millisecond steps, where recording them would be
+# part of what is timed)
 SWEEP = [
-    ("single4096_h4_d128", [4096], 4, 50, 5),
-    ("single16384_h4_d128", [16384], 4, 20, 3),
-    ("single131072_h4_d128", [131072], 4, 5, 2),
-    ("single638976_h4_d128", [638976], 4, 3, 1),
-    ("packed65536_loguniform128-8192_h32_d128", None, 32, 10, 3),
+    ("single4096_h4_d128", [4096], 4, 50, 5, False),
+    ("single16384_h4_d128", [16384], 4, 20, 3, False),
+    ("single131072_h4_d128", [131072], 4, 5, 2, True),
+    ("single638976_h4_d128", [638976], 4, 3, 1, True),
+    ("packed65536_loguniform128-8192_h32_d128", None, 32, 10, 3, True),
 ]
 
 
@@ -201,12 +203,12 @@ def sweep(main_name: str, main_ms: float, main_kms: dict, main_steps: int, main_
     from paper_2511_13198_amd import accounting as acc
     from paper_2511_13198_amd import workloads as wl
     out = []
-    for label, lengths, heads, steps, warmup in SWEEP:
+    for label, lengths, heads, steps, warmup, events in SWEEP:
         w = wl.config(2) if lengths is None else wl.Workload(label, lengths, heads, heads, 128)
         if w.name == main_name:
             ms, kms, steps, warmup = main_ms, main_kms, main_steps, main_warmup
         else:
-            ms, kms, inputs = time_steps(w, steps, warmup, events_in_timed=False)
+            ms, kms, inputs = time_steps(w, steps, warmup, events_in_timed=events)
             del inputs
             torch.cuda.empty_cache()
         flops = acc.fwd_bwd_flops(w.lengths, w.heads_q, w.head_dim, w.causal)
