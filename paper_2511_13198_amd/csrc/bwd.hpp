@@ -5,11 +5,11 @@
 //   dQ = scale * dS K.
 // Three kernels:
 //   * bwd_pre_kernel    D = rowsum(dO * O) (fp32, [Hq, T]) -- bandwidth bound.
-//   * bwd_dkdv_kernel   one workgroup per (segment, kv head, 128-key tile); a
-//                       pair of waves owns 32 keys (K and V tiles in LDS),
-//                       keeps dK^T / dV^T in accumulators, and sweeps every
-//                       query head of the group and every 64-row query step
-//                       that sees the keys.  Written once, no atomics.
+//   * bwd_dkdv_kernel   one workgroup per (segment, kv head, 256-key tile); a
+//                       wave owns 32 keys (K in an LDS tile, V in registers),
+//                       keeps their dK^T / dV^T in accumulators, and sweeps
+//                       every query head of the group and every 64-row query
+//                       step that sees the keys.  Written once, no atomics.
 //   * bwd_dq_kernel     one workgroup per (segment, query head, 32-row-per-wave
 //                       tile); mirrors the forward: recomputes S^T and dP^T,
 //                       forms dS^T and accumulates dQ^T = K^T dS^T.  No atomics.
@@ -124,29 +124,30 @@ struct BwdArgs {
   float* part_dq;
 };
 
-// dK/dV: one workgroup of 8 waves per (segment, kv head, 128-key tile).  Waves
-// w and w+4 own the same 32 keys (K and V read as B operands from LDS tiles
-// shared by the workgroup) and split every 64-row query step: wave w takes rows
-// 0..31, wave w+4 rows 32..63.  Two waves per SIMD let one wave's softmax
-// recomputation overlap the other's matrix products.  The pair's dK^T/dV^T
-// accumulators are summed through LDS once at the end.  Under split-K a
-// workgroup takes one contiguous part of the tile's query steps and writes
-// partial dK/dV for split_sum_kernel.
+// dK/dV: one workgroup of 8 waves per (segment, kv head, 256-key tile).  Wave
+// w owns keys 32w..32w+31 of the tile alone: its dK^T / dV^T accumulators,
+// its V fragments (held in registers as the B operand of dP) and its K rows
+// (in an LDS tile, read as the B operand of S).  Every wave sweeps the same
+// 64-row query steps, taking each as two 32-row halves, so the Q/dO tile of a
+// step is shared by all eight waves and one barrier covers 64 matrix products
+// per wave.  Two waves per SIMD let one wave's softmax recomputation overlap
+// the other's matrix products.  Under split-K a workgroup takes one
+// contiguous part of the tile's query steps and writes partial dK/dV for
+// split_sum_kernel.
 template <int D>
 struct DkdvCfg {
-  static constexpr int BK = 128;  // keys per workgroup (32 per wave pair)
-  static constexpr int BQ = 64;   // query rows per step (32 per wave)
   static constexpr int NW = 8;
+  static constexpr int BK = 32 * NW;  // keys per workgroup (32 per wave)
+  static constexpr int BQ = 64;       // query rows per step (two halves of 32)
   static constexpr int NT = NW * 64;
   using QL = DualLayout<D>;  // Q and dO: read as rows (S, dP) and transposed (dK, dV)
-  using KL = RowsLayout<D>;  // K and V: read as rows only
+  using KL = RowsLayout<D>;  // K: read as rows only
   static constexpr int QTILE = QL::elems(BQ);
   static constexpr int KTILE = KL::elems(BK);
   // per stage: Q tile, dO tile, lse2[BQ], D[BQ]
   static constexpr int STAGE = 2 * QTILE * 2 + 2 * BQ * 4;
-  static constexpr int MAIN_BYTES = 2 * STAGE + 2 * KTILE * 2;
-  static constexpr int RED_BYTES = 4 * 32 * D * 2 * 4;  // 4 pairs x (dK, dV) fp32
-  static constexpr int LDS_BYTES = MAIN_BYTES > RED_BYTES ? MAIN_BYTES : RED_BYTES;
+  static constexpr int LDS_BYTES = 2 * STAGE + KTILE * 2;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS of one CU");
 };
 
 template <int D>
@@ -183,11 +184,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
 
   const int l = __lane_id();
   const int w = threadIdx.x >> 6;
-  const int pw = w & 3;    // key block of the pair
-  const int half = w >> 2; // which 32 rows of each step
   const int hh = l >> 5;
-  const int kw0 = k0 + pw * 32;        // first key of this wave
-  const int key = kw0 + (l & 31);      // this lane's key
+  const int kw0 = k0 + w * 32;    // first key of this wave
+  const int key = kw0 + (l & 31);  // this lane's key
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
 
@@ -197,10 +196,17 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     dka[i] = zero16();
     dva[i] = zero16();
   }
+  // V^T as B operand of dP = dO V^T: lane holds V[key][ks*16 + hh*8 + j]
+  // (keys past the segment end are zeros; their gradients are never written)
+  bf16x8 vf[D / 16];
+  {
+    const uint16_t* vp = a.v + (size_t)key * kvstride + (size_t)hk * D + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) vf[ks] = load_bf16x8(vp + ks * 16, key < k_hi);
+  }
 
   uint8_t* const base = reinterpret_cast<uint8_t*>(smem);
   uint16_t* const ktile_s = reinterpret_cast<uint16_t*>(base + 2 * C::STAGE);
-  uint16_t* const vtile = ktile_s + C::KTILE;
   auto qbuf = [&](int b) __attribute__((always_inline)) {
     return reinterpret_cast<uint16_t*>(base + b * C::STAGE);
   };
@@ -258,46 +264,45 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int q_tr = tr_lane_base<QL>();
   const int k_row = row_lane_base<KL>();
 
-  // returns false for a wave with nothing to do in this step; `hook(KS)` runs
-  // after the products of K-step KS of S/dP (active waves only)
-  auto compute = [&](int step, const StepPos& p, auto&& hook) __attribute__((always_inline)) {
+  // Half `hf` (rows 32 hf .. 32 hf + 31) of a step.  Returns false for a wave
+  // with nothing to do there; `hook(KS)` runs after the products of K-step KS
+  // of S/dP (active waves only)
+  auto compute = [&](int step, const StepPos& p, int hf, auto&& hook) __attribute__((always_inline)) {
     const int b = step & 1;
     const uint16_t* qs = qbuf(b);
     const uint16_t* gs = gbuf(b);
     const float* lse_s = stats(b);
     const float* dd_s = lse_s + BQ;
-    const int wr0 = p.r0 + half * 32;  // first row of this wave
+    const int wr0 = p.r0 + hf * 32;  // first row of this half
     const bool active = (kw0 < k_hi) && (wr0 < q_hi) && (!a.causal || wr0 + 31 + shift >= kw0);
     if (!active) return false;
     const bool need_mask = (a.causal && wr0 + shift < kw0 + 31) || (wr0 + 32 > q_hi);
-    // S[row][key] = Q K^T and dP[row][key] = dO V^T for the wave's 32 rows;
-    // the four operand fragments of a K-step are read PIPE steps ahead
+    // S[row][key] = Q K^T and dP[row][key] = dO V^T for the half's 32 rows;
+    // the Q, K and dO fragments of a K-step are read PIPE steps ahead
     f32x16 s = zero16(), dp = zero16();
     {
       constexpr int NKS = D / 16, PIPE = PDY_DKDV_PIPE;
-      const uint32_t qa = lds_addr(qs) + (q_row + half * 32 * QL::ROW) * 2;
-      const uint32_t ga = lds_addr(gs) + (q_row + half * 32 * QL::ROW) * 2;
-      const uint32_t ka = lds_addr(ktile_s) + (k_row + pw * 32 * KL::ROW) * 2;
-      const uint32_t va = lds_addr(vtile) + (k_row + pw * 32 * KL::ROW) * 2;
-      u32x4 rq[PIPE + 1], rk[PIPE + 1], rg[PIPE + 1], rv[PIPE + 1];
+      const uint32_t qa = lds_addr(qs) + (q_row + hf * 32 * QL::ROW) * 2;
+      const uint32_t ga = lds_addr(gs) + (q_row + hf * 32 * QL::ROW) * 2;
+      const uint32_t ka = lds_addr(ktile_s) + (k_row + w * 32 * KL::ROW) * 2;
+      u32x4 rq[PIPE + 1], rk[PIPE + 1], rg[PIPE + 1];
       auto rd = [&](auto KS) __attribute__((always_inline)) {
         constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
         row_issue<QL, 0, ks * 16>(qa, rq[sl]);
         row_issue<KL, 0, ks * 16>(ka, rk[sl]);
         row_issue<QL, 0, ks * 16>(ga, rg[sl]);
-        row_issue<KL, 0, ks * 16>(va, rv[sl]);
       };
       static_for<PIPE>([&](auto KS) { rd(KS); });
       static_for<NKS>([&](auto KS) {
         constexpr int ks = decltype(KS)::value, sl = ks % (PIPE + 1);
         if constexpr (ks + PIPE < NKS) {
           rd(std::integral_constant<int, ks + PIPE>{});
-          row_wait<4 * PIPE>(rq[sl], rk[sl], rg[sl], rv[sl]);
+          row_wait<3 * PIPE>(rq[sl], rk[sl], rg[sl]);
         } else {
-          row_wait<4 * (NKS - 1 - ks)>(rq[sl], rk[sl], rg[sl], rv[sl]);
+          row_wait<3 * (NKS - 1 - ks)>(rq[sl], rk[sl], rg[sl]);
         }
         s = mfma32(as_bf16x8(rq[sl]), as_bf16x8(rk[sl]), s);
-        dp = mfma32(as_bf16x8(rg[sl]), as_bf16x8(rv[sl]), dp);
+        dp = mfma32(as_bf16x8(rg[sl]), vf[ks], dp);
         hook(KS);
       });
     }
@@ -313,7 +318,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp) {
-      const int rl = half * 32 + grp * 8 + hh * 4;
+      const int rl = hf * 32 + grp * 8 + hh * 4;
       const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rl);
       const f32x4 d4 = *reinterpret_cast<const f32x4*>(dd_s + rl);
 #pragma unroll
@@ -327,8 +332,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
     // dV^T += dO^T P  and  dK^T += Q^T dS over two 16-row steps; the
     // transposing reads of the next product are in flight during each one
     constexpr int NDB = D / 32;
-    const uint32_t ga = lds_addr(gs) + (q_tr + half * 32 * QL::ROW) * 2;
-    const uint32_t qa = lds_addr(qs) + (q_tr + half * 32 * QL::ROW) * 2;
+    const uint32_t ga = lds_addr(gs) + (q_tr + hf * 32 * QL::ROW) * 2;
+    const uint32_t qa = lds_addr(qs) + (q_tr + hf * 32 * QL::ROW) * 2;
     TrRegs ra[NDB], rb[NDB];
     // the two waves of a SIMD run the same phases at about the same time;
     // raising the priority of a wave in this product-only phase lets it keep
@@ -363,15 +368,14 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   };
   auto rows_valid = [&](const StepPos& p) __attribute__((always_inline)) { return q_hi - p.r0; };
 
-  // K and V tiles: keys past the segment end read as zeros (the copies'
-  // range check); their gradients are never written out.  Query-side rows
-  // past the segment end likewise, and are masked.
+  // The K tile: keys past the segment end read as zeros (the copies' range
+  // check); their gradients are never written out.  Query-side rows past the
+  // segment end likewise, and are masked.
   {
     {
-      TileDma<KL, BK, NW> kvd;
-      kvd.init(kvstride);
-      kvd.issue(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, ktile_s);
-      kvd.issue(a.v + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, vtile);
+      TileDma<KL, BK, NW> kd;
+      kd.init(kvstride);
+      kd.issue(a.k + (size_t)k0 * kvstride + (size_t)hk * D, kvstride, k_hi - k0, ktile_s);
     }
     using QD = TileDma<QL, BQ, NW>;
     constexpr int PQ = QD::PER_WAVE;  // copies of one tile per wave (at most)
@@ -397,14 +401,15 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       store_stat(step & 1);
       __syncthreads();
       if (more) load_stat(nxt);
-      // the next step's copies go out one per K-step of S/dP, so that they
-      // trickle into the memory pipeline instead of stalling every wave at once
-      // (built for every step; only used when there is a next one)
+      // the next step's copies go out one per K-step of the first half's
+      // S/dP, so that they trickle into the memory pipeline instead of
+      // stalling every wave at once (built for every step; only used when
+      // there is a next one)
       const int rvn = rows_valid(nxt);
       const typename QD::Src rsq = QD::src(row_ptr(a.q, nxt), qstride, rvn);
       const typename QD::Src rsg = QD::src(row_ptr(a.dout, nxt), qstride, rvn);
       const int bn = (step + 1) & 1;
-      const bool ran = compute(step, cur, [&](auto KS) __attribute__((always_inline)) {
+      const bool ran = compute(step, cur, 0, [&](auto KS) __attribute__((always_inline)) {
         constexpr int c = decltype(KS)::value;
         if constexpr (c < PQ) {
           if (more) qd.issue_one(c, rsq, qbuf(bn));
@@ -413,28 +418,15 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
         }
       });
       if (!ran && more) issue(step + 1, nxt);
+      compute(step, cur, 1, [](auto) {});
       cur = nxt;
     }
   }
 
-  // sum the pair's accumulators: waves 4..7 park theirs in LDS, over the
-  // K/V and Q/dO tiles.  Every copy this wave issued must have landed first
-  // (a part with no query steps still issued its K/V copies), then the
-  // barrier orders the other waves' copies and reads before the stores.
+  // every copy this wave issued has landed before the workgroup ends (a part
+  // with no query steps still issued its K copies)
   wait_dma();
-  __syncthreads();
-  float* red = reinterpret_cast<float*>(base) + pw * (32 * D * 2);
-  if (half == 1) {
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        red[(db * 16 + r) * 64 + l] = dka[db][r];
-        red[32 * D + (db * 16 + r) * 64 + l] = dva[db][r];
-      }
-  }
-  __syncthreads();
-  if (half == 0 && key < k_hi) {
+  if (key < k_hi) {
     const bool split = a.nsplit_kv > 1;
     const size_t off = (size_t)key * kvstride + (size_t)hk * D;
     const size_t poff = (size_t)part * (a.chunked ? a.tk : a.total_tokens) * kvstride + off;
@@ -449,8 +441,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = grp * 4 + e;
-          kv[e] = (dka[db][r] + red[(db * 16 + r) * 64 + l]) * a.scale;
-          vv[e] = dva[db][r] + red[32 * D + (db * 16 + r) * 64 + l];
+          kv[e] = dka[db][r] * a.scale;
+          vv[e] = dva[db][r];
         }
         if (a.accumulate && !split) {
           kv += *reinterpret_cast<const f32x4*>(dkp + d0);

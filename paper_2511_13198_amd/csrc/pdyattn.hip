@@ -31,13 +31,15 @@ pdy_status hip_fail(hipError_t e, const char* what) {
   return fail(PDY_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr int kTile = 128;  // schedule granularity of the backward kernels
+constexpr int kTile = 128;  // smallest tile of any kernel (bounds the work items)
+constexpr int kKvTile = pdy::DkdvCfg<128>::BK;  // keys per dK/dV work item
+static_assert(pdy::DkdvCfg<64>::BK == kKvTile, "one key-tile schedule for both head dims");
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 struct Sizes {
   int64_t T, N, maxlen, hq, hkv, d;
-  int max_nt;  // tiles of kTile in the longest segment
+  int max_nt;  // tiles of kTile in the longest segment (unused by the launches)
 };
 
 int tiles_of(const Sizes& s, int tile) {
@@ -222,9 +224,9 @@ int dq_split(const Sizes& sq, const Sizes& sk) {
 // the heaviest key tile visits every 64-row query step of every head of its group
 int dkdv_split(const Sizes& sq, const Sizes& sk) {
   const int rows = pdy::DkdvCfg<128>::BQ;
-  return split_parts(grid_items(sk, kTile) * sk.hkv,
+  return split_parts(grid_items(sk, kKvTile) * sk.hkv,
                      (int64_t)tiles_of(sq, rows) * (sq.hq / sq.hkv),
-                     tile_us((double)rows * kTile, sq, 8.0, 4.5),
+                     tile_us((double)rows * kKvTile, sq, 8.0, 4.5),
                      2.0 * sk.T * sk.hkv * sk.d * 4);
 }
 
@@ -246,7 +248,7 @@ size_t bwd_split_bytes(const Sizes& sq, const Sizes& sk) {
 
 // workspace of a (non-chunk) backward: both tile schedules, D and any split-K partials
 size_t bwd_workspace_bytes(const Sizes& s) {
-  return plan_bytes(s, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
+  return plan_bytes(s, kKvTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
          bwd_split_bytes(s, s);
 }
 
@@ -471,7 +473,7 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
 
 // sk: sizes of the key side (the query side for self-attention)
 size_t bwd_need(const Sizes& s, const Sizes& sk) {
-  return plan_bytes(sk, kTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s);
+  return plan_bytes(sk, kKvTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s);
 }
 
 pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, const float* lse,
@@ -507,15 +509,15 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   int32_t* ws = reinterpret_cast<int32_t*>(workspace);
   int32_t* ws_q = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) +
-                                              plan_bytes(sk, kTile));
+                                              plan_bytes(sk, kKvTile));
   float* dd = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace) +
-                                       plan_bytes(sk, kTile) + plan_bytes(s, qtile));
+                                       plan_bytes(sk, kKvTile) + plan_bytes(s, qtile));
 
   {
     // the query-tile schedule, and the key-tile one unless there are no keys
     // (the key side has the same segments as the query side, or is a chunk)
     const pdy::PlanJob q_job = plan_job(cu, ws_q, s, qtile);
-    const pdy::PlanJob kv_job = plan_job(cu, ws, sk, kTile);
+    const pdy::PlanJob kv_job = plan_job(cu, ws, sk, kKvTile);
     if (needs_plan(s) &&
         (st = launch_plans(q_job, sk.T > 0 ? &kv_job : nullptr, hs)) != PDY_OK)
       return st;
@@ -546,7 +548,7 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   a.dq = dq;
   a.dk = dk;
   a.dv = dv;
-  a.plan = make_plan(ws, sk, kTile);
+  a.plan = make_plan(ws, sk, kKvTile);
   a.plan_q = make_plan(ws_q, s, qtile);
   a.total_tokens = (int)s.T;
   a.hq = (int)s.hq;
@@ -581,7 +583,7 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     });
   };
   if (sk.T > 0) {
-    const dim3 gkv((unsigned)(grid_items(sk, kTile) * s.hkv * nsplit_kv));
+    const dim3 gkv((unsigned)(grid_items(sk, kKvTile) * s.hkv * nsplit_kv));
     e = launch_timed(K_DKDV, hs, [&] {
       if (s.d == 64)
         hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),

@@ -110,13 +110,13 @@ MiB = 1 << 20
 def test_split_k_workspace():
     """Launches too small to fill the chip split their work (split-K) and need
     fp32 partial buffers; the size queries make the same decision as the
-    calls.  8192 tokens x 4 heads: forward and dQ in 4 parts, dK/dV in 2."""
+    calls.  8192 tokens x 4 heads: forward, dQ and dK/dV in 4 parts."""
     part_o = 4 * 8192 * 4 * 128 * 4
     assert P.fwd_workspace_size(8192, 1, 8192, 4, 4, 128) >= part_o + 4 * 4 * 8192 * 4
-    assert P.bwd_workspace_size(8192, 1, 8192, 4, 4, 128) >= 2 * (2 * 8192 * 4 * 128 * 4) + part_o
-    # grouped heads at 16K: only dK/dV (2 kv heads) splits, in 2 parts
+    assert P.bwd_workspace_size(8192, 1, 8192, 4, 4, 128) >= 2 * (4 * 8192 * 4 * 128 * 4) + part_o
+    # grouped heads at 16K: only dK/dV (2 kv heads: 128 key tiles) splits, in 4 parts
     b = P.bwd_workspace_size(16384, 1, 16384, 8, 2, 128)
-    assert 2 * (2 * 16384 * 2 * 128 * 4) <= b < 2 * (2 * 16384 * 2 * 128 * 4) + 2 * MiB
+    assert 2 * (4 * 16384 * 2 * 128 * 4) <= b < 2 * (4 * 16384 * 2 * 128 * 4) + 2 * MiB
     # launches that fill the chip need no partial buffers
     assert P.fwd_workspace_size(131072, 1, 131072, 4, 4, 128) < MiB
     assert P.bwd_workspace_size(16384, 1, 16384, 8, 8, 64) < 2 * MiB
