@@ -22,16 +22,18 @@
 
 namespace pdy {
 
-// dst = (accumulate ? dst : 0) + sum_p parts[p * n + i] over the nsplit
-// partial gradients of a split-K backward, in part order, for one array
+// dst = (accumulate ? dst : 0) + sum_p parts[p * n + i] over the partial
+// gradients of a split-K backward, in part order, for one array
 // (parts_b == nullptr) or two of the same size (dK and dV in one launch:
 // the grid's second half takes the second); 4 floats per thread (n is a
-// multiple of 4: a head dimension of 64 or 128 divides it).
+// multiple of 4: a head dimension of 64 or 128 divides it).  Element i
+// belongs to query row or key i / row_elems, which has sp.nparts of its
+// item.
 __global__ void __launch_bounds__(256) split_sum_kernel(const float* __restrict__ parts_a,
                                                         float* __restrict__ dst_a,
                                                         const float* __restrict__ parts_b,
-                                                        float* __restrict__ dst_b, int nsplit,
-                                                        size_t n, int accumulate) {
+                                                        float* __restrict__ dst_b, Split sp,
+                                                        size_t n, int row_elems, int accumulate) {
   size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   const float* parts = parts_a;
   float* dst = dst_a;
@@ -42,6 +44,7 @@ __global__ void __launch_bounds__(256) split_sum_kernel(const float* __restrict_
     parts = parts_b;
     dst = dst_b;
   }
+  const int nsplit = sp.nparts(sp.item_of((int)(i / row_elems)));
   f32x4 acc = accumulate ? *reinterpret_cast<const f32x4*>(dst + i) : f32x4{0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < nsplit; ++p) acc += *reinterpret_cast<const f32x4*>(parts + p * n + i);
   *reinterpret_cast<f32x4*>(dst + i) = acc;
@@ -111,14 +114,14 @@ struct BwdArgs {
   int tk;
   int shift;
   int accumulate;  // add to dq/dk/dv instead of overwriting them
-  // split-K (nsplit_* > 1): the work of every dK/dV key tile (its query
+  // split-K (split_*.parts > 1): the work of every dK/dV key tile (its query
   // steps) or dQ query tile (its key tiles) is cut into contiguous parts, one
-  // workgroup each, and a part writes its scaled partial gradient to
-  // part_dk/part_dv [nsplit_kv][keys][Hkv][D] or part_dq [nsplit_q][T][Hq][D]
+  // workgroup each, and part p writes its scaled partial gradient to
+  // part_dk/part_dv [parts][keys][Hkv][D] or part_dq [parts][T][Hq][D]
   // (fp32, never accumulated; keys = tk for a chunk, else T) for
   // split_sum_kernel to add up.
-  int nsplit_kv;
-  int nsplit_q;
+  Split split_kv;
+  Split split_q;
   float* part_dk;
   float* part_dv;
   float* part_dq;
@@ -164,10 +167,9 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   // its L2 (with 2 kv heads and plain round-robin, each XCD would stream
   // every fourth key tile's rows: an 8 MB window and 20x the traffic beyond
   // L2)
-  int hk, entry;
+  int hk, entry, item, part, nparts;
   xcd_order(blockIdx.x, gridDim.x, a.hkv, hk, entry);
-  const int item = entry / a.nsplit_kv;
-  const int part = entry % a.nsplit_kv;
+  if (!split_entry(a.split_kv, entry, item, part, nparts)) return;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
   // keys [k_lo, k_hi) (this workgroup: a tile of them), query rows
@@ -219,8 +221,8 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int qstart = a.causal ? max(q_lo, k0 - shift) : q_lo;
   const int nqt = max(0, (q_hi - qstart + BQ - 1) / BQ);
   // this part's steps [s_begin, s_begin + nsteps) of the tile's nqt * g
-  const int s_begin = part * (nqt * g) / a.nsplit_kv;
-  const int nsteps = (part + 1) * (nqt * g) / a.nsplit_kv - s_begin;
+  const int s_begin = part * (nqt * g) / nparts;
+  const int nsteps = (part + 1) * (nqt * g) / nparts - s_begin;
   // a step is one BQ-row tile of one query head of the group: the head's
   // tiles from the last row down to the key tile (the causal diagonal comes
   // last), then the next head's; tracked incrementally (no division in the
@@ -427,7 +429,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   // with no query steps still issued its K copies)
   wait_dma();
   if (key < k_hi) {
-    const bool split = a.nsplit_kv > 1;
+    const bool split = a.split_kv.parts > 1;
     const size_t off = (size_t)key * kvstride + (size_t)hk * D;
     const size_t poff = (size_t)part * (a.chunked ? a.tk : a.total_tokens) * kvstride + off;
     float* dkp = split ? a.part_dk + poff : a.dk + off;
@@ -476,10 +478,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
 
   // workgroup -> (head, work item, part of its key tiles), in the XCD-aware
   // order, as in the forward
-  int h, entry;
+  int h, entry, item, part, nparts;
   xcd_order(blockIdx.x, gridDim.x, a.hq, h, entry);
-  const int item = entry / a.nsplit_q;
-  const int part = entry % a.nsplit_q;
+  if (!split_entry(a.split_q, entry, item, part, nparts)) return;
   int seg, level;
   if (!plan_lookup(a.plan_q, item, seg, level)) return;
   // query rows [seg_lo, seg_hi), keys [k_lo, k_hi); causal: key j visible to
@@ -527,8 +528,8 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const int kv_end = a.causal ? min(k_hi, q0 + BQ + shift) : k_hi;
   const int ntiles = max(0, (kv_end - k_lo + BK - 1) / BK);
   // this part's key tiles [t_begin, t_end) (possibly none)
-  const int t_begin = part * ntiles / a.nsplit_q;
-  const int t_end = (part + 1) * ntiles / a.nsplit_q;
+  const int t_begin = part * ntiles / nparts;
+  const int t_end = (part + 1) * ntiles / nparts;
   auto kbuf = [&](int t) __attribute__((always_inline)) { return smem + (t & 1) * C::KTILE; };
   auto vbuf = [&](int t) __attribute__((always_inline)) {
     return smem + 2 * C::KTILE + (t & 1) * C::VTILE;
@@ -655,7 +656,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   }
 
   if (row < seg_hi) {
-    const bool split = a.nsplit_q > 1;
+    const bool split = a.split_q.parts > 1;
     const size_t off = (size_t)row * qstride + (size_t)h * D;
     float* dqp = split ? a.part_dq + (size_t)part * a.total_tokens * qstride + off : a.dq + off;
 #pragma unroll

@@ -388,6 +388,101 @@ __device__ __forceinline__ void xcd_order(int b, int n, int nheads, int& head, i
   entry = (r * g + blk) * kPer + q;
 }
 
+// Split-K of a launch whose work items cannot fill the chip: each item's
+// inner loop (its units: the key tiles of a query tile, or the query steps of
+// a key tile over the query heads of its group) is cut into contiguous parts,
+// one workgroup each, whose partial results a second kernel combines.
+//   * uniform (cap == 0): every item in `parts` parts;
+//   * balanced (cap > 0, single-segment launches only): item i (the i-th
+//     heaviest) in ceil(units(i) / cap) parts, so that light items are not
+//     cut into slivers while the heaviest sets the launch's time; `parts` is
+//     then the most parts of any item (the number of partial slices).
+// A part p of an item with n parts and u units takes units
+// [p u / n, (p + 1) u / n).
+struct Split {
+  int parts;
+  int cap;
+  int kind;    // 0: items are query tiles of `rows` rows, units key tiles of `keys`
+               // 1: items are key tiles of `keys` keys, units steps of `rows` rows
+  int nitems;  // items per head (balanced)
+  int total;   // tokens of the segment (balanced)
+  int causal;
+  int rows, keys;
+  int group;   // query heads per kv head (kind 1)
+
+  // units of inner work of item i (balanced), i = 0 the heaviest
+  __host__ __device__ int units(int i) const {
+    if (kind == 0) {
+      const int q0 = (nitems - 1 - i) * rows;
+      const int kv_end = causal ? (q0 + rows < total ? q0 + rows : total) : total;
+      return (kv_end + keys - 1) / keys;
+    }
+    const int qstart = causal ? i * keys : 0;
+    return (total - qstart + rows - 1) / rows * group;
+  }
+  __host__ __device__ int nparts(int i) const { return cap ? (units(i) + cap - 1) / cap : parts; }
+  // item of the query row (kind 0) or key (kind 1) at `pos`
+  __host__ __device__ int item_of(int pos) const {
+    return kind == 0 ? nitems - 1 - pos / rows : pos / keys;
+  }
+};
+
+// Item, part and part count of workgroup `entry` (of one head) under split
+// sp.  Balanced: the parts of an item are consecutive entries, heavier items
+// first; one pass of the wave over the items (a split launch has fewer than
+// 512 items) finds the entry's item.  Returns false past the last part.  All
+// results are wave-uniform.
+__device__ __forceinline__ bool split_entry_scan(const Split& sp, int entry, int& item, int& part,
+                                                 int& nparts);
+__device__ __forceinline__ bool split_entry(const Split& sp, int entry, int& item, int& part,
+                                            int& nparts) {
+  bool ok = true;
+  if (sp.cap == 0) {
+    item = entry / sp.parts;
+    part = entry % sp.parts;
+    nparts = sp.parts;
+  } else {
+    ok = split_entry_scan(sp, entry, item, part, nparts);
+  }
+  // wave-uniform: kept in scalar registers
+  item = __builtin_amdgcn_readfirstlane(item);
+  part = __builtin_amdgcn_readfirstlane(part);
+  nparts = __builtin_amdgcn_readfirstlane(nparts);
+  return ok;
+}
+__device__ __forceinline__ bool split_entry_scan(const Split& sp, int entry, int& item, int& part,
+                                                 int& nparts) {
+  const int l = __lane_id();
+  const int per = (sp.nitems + 63) >> 6;  // items per lane
+  int mine = 0;
+  for (int k = 0; k < per; ++k) {
+    const int i = l * per + k;
+    if (i < sp.nitems) mine += sp.nparts(i);
+  }
+  int incl = mine;  // inclusive prefix sum over the lanes
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_up(incl, off);
+    if (l >= off) incl += t;
+  }
+  const unsigned long long hit = __ballot(entry >= incl - mine && entry < incl);
+  if (hit == 0) return false;
+  const int src = __ffsll((long long)hit) - 1;  // the lane whose items hold the entry
+  int base = __shfl(incl - mine, src);
+  for (int k = 0; k < per; ++k) {
+    const int i = src * per + k;
+    const int n = sp.nparts(i);
+    if (entry < base + n) {
+      item = i;
+      part = entry - base;
+      nparts = n;
+      return true;
+    }
+    base += n;
+  }
+  return false;
+}
+
 __device__ __forceinline__ bool plan_lookup(const Plan& p, int item, int& seg, int& level) {
   if (p.order == nullptr) {  // one segment: item i is its level max_nt - 1 - i
     if (item >= p.max_nt) return false;

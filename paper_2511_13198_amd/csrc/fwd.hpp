@@ -76,12 +76,12 @@ struct FwdArgs {
   int chunked;
   int tk;
   int shift;
-  // split-K (nsplit > 1): the key tiles of every query tile are cut into
-  // nsplit contiguous parts, one workgroup each; a part writes its O (fp32,
-  // normalised by its own row sums) to part_o [nsplit][T][Hq][D] and its LSE
-  // to part_lse [nsplit][Hq][T] instead of o / lse, and split_merge_kernel
-  // combines them.  nsplit = 1: o and lse directly.
-  int nsplit;
+  // split-K (split.parts > 1): the key tiles of every query tile are cut into
+  // contiguous parts, one workgroup each; part p writes its O (fp32,
+  // normalised by its own row sums) to part_o [parts][T][Hq][D] and its LSE
+  // to part_lse [parts][Hq][T] instead of o / lse, and split_merge_kernel
+  // combines them.  split.parts = 1: o and lse directly.
+  Split split;
   float* part_o;
   float* part_lse;
 };
@@ -104,7 +104,7 @@ __device__ __forceinline__ void fwd_epilogue(const FwdArgs& a, const f32x16 (&oa
   const bool seen = ltot > 0.f;
   const float inv = seen ? 1.f / ltot : 0.f;
   const float lse = seen ? (m + __builtin_log2f(ltot)) * kLn2 : -INFINITY;
-  if (a.nsplit > 1) {
+  if (a.split.parts > 1) {
     float* op = a.part_o + ((size_t)part * a.total_tokens + row) * qstride + (size_t)h * D;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -144,10 +144,9 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   // in the XCD-aware order: the workgroups an XCD runs at a time hold
   // neighbouring query tiles of one head, which stream the same K/V tiles
   // from key 0 and finish close together (4 heads: 1.4 % faster)
-  int h, entry;
+  int h, entry, item, part, nparts;
   xcd_order(blockIdx.x, gridDim.x, a.hq, h, entry);
-  const int item = entry / a.nsplit;
-  const int part = entry % a.nsplit;
+  if (!split_entry(a.split, entry, item, part, nparts)) return;
   int seg, level;
   if (!plan_lookup(a.plan, item, seg, level)) return;
   // query rows [seg_lo, seg_hi), keys [k_lo, k_hi); causal: key j visible to
@@ -191,8 +190,8 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const int kv_end = a.causal ? min(k_hi, q0 + BQ + shift) : k_hi;
   const int ntiles = max(0, (kv_end - k_lo + BK - 1) / BK);
   // this part's key tiles [t_begin, t_end) (possibly none)
-  const int t_begin = part * ntiles / a.nsplit;
-  const int t_end = (part + 1) * ntiles / a.nsplit;
+  const int t_begin = part * ntiles / nparts;
+  const int t_end = (part + 1) * ntiles / nparts;
 
   auto kbuf = [&](int t) __attribute__((always_inline)) {
     return smem + (t % C::STAGES) * (C::KTILE + C::VTILE);
@@ -426,15 +425,16 @@ __global__ void __launch_bounds__(256) merge_kernel(const uint16_t* oa, const fl
   if (sub == 0) lse[li] = l;
 }
 
-// Combine the nsplit parts of a split-K forward (each over its own key
-// range of the same rows), by the same rule as merge_kernel:
+// Combine the parts of a split-K forward (each over its own key range of
+// the same rows; a row has sp.nparts of its query tile), by the same rule as
+// merge_kernel:
 //   LSE = log sum_p exp(LSE_p),  O = sum_p exp(LSE_p - LSE) O_p,
 // parts with LSE = -inf weigh nothing and a row where every part is -inf
 // gets O = 0, LSE = -inf.  Parts are fp32, O is rounded to bf16 once.  One
 // 8-element slice of a row and head per thread.
 template <int D>
 __global__ void __launch_bounds__(256) split_merge_kernel(const float* part_o,
-                                                          const float* part_lse, int nsplit,
+                                                          const float* part_lse, Split sp,
                                                           uint16_t* o, float* lse,
                                                           int total_tokens, int hq) {
   constexpr int LANES = D / 8;
@@ -446,6 +446,7 @@ __global__ void __launch_bounds__(256) split_merge_kernel(const float* part_o,
   const size_t row = pair / hq;
   const int h = (int)(pair % hq);
   const size_t li = (size_t)h * total_tokens + row;
+  const int nsplit = sp.nparts(sp.item_of((int)row));
   float mx = -INFINITY;
   for (int p = 0; p < nsplit; ++p) mx = fmaxf(mx, part_lse[p * rows + li]);
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};

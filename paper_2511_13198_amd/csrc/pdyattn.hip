@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -205,29 +206,145 @@ double tile_us(double pairs, const Sizes& s, double flops_per_pair_d, double tfl
   return pairs * flops_per_pair_d * (double)s.d / (tflops * 1e6);
 }
 
-// sq: the query rows' sizes; sk: the keys' (the same for self-attention
-// over cu's segments, one chunk each for a context-parallel pair)
-int fwd_split(const Sizes& sq, const Sizes& sk) {
-  const int rows = 32 * fwd_waves(sq), keys = fwd_key_tile(sq);
-  return split_parts(grid_items(sq, rows) * sq.hq, tiles_of(sk, keys),
-                     tile_us((double)rows * keys, sq, 4.0, 4.5),
-                     (double)sq.T * sq.hq * sq.d * 4);
+// A split of `p` parts per item (p = 1: none).
+pdy::Split uniform_split(int p) {
+  pdy::Split sp{};
+  sp.parts = p;
+  sp.cap = 0;
+  sp.rows = sp.keys = sp.group = 1;
+  return sp;
 }
 
-int dq_split(const Sizes& sq, const Sizes& sk) {
+constexpr int64_t kCUs = 256;  // compute units of the chip
+constexpr int kMaxParts = 16;  // partial slices of a balanced split at most
+
+// Balanced split-K of a causal single-segment launch whose uniform split
+// takes p > 1 parts per item.  Under the causal mask the items' units range
+// from one to the heaviest item's, so equal part counts leave the heaviest
+// item's parts (which set the launch's time) several times the mean part; a
+// balanced split gives the heaviest items more parts and light items fewer.
+// It is taken only when the uniform split's workgroups fit one round on the
+// chip (one per CU): over two rounds the uniform parts, dealt heaviest first,
+// already pair a heavy part with a light one on each CU, which balanced parts
+// (ordered by item, not by size) do not (8K tokens x 4 heads: 607 against 567
+// TFLOP/s).  For a budget of workgroups (over the heads) the smallest cap
+// (units per part) that fits it is found by bisection (O(items log units) on
+// the host; items < 256 here), with at most kMaxParts slices.  Two budgets
+// are tried, the uniform split's workgroup count and one workgroup per CU,
+// and the one with the lower estimated time is kept: the heaviest part or the
+// mean load per CU, whichever is larger, at unit_us per unit, plus the
+// partial results written and read back (slice_bytes for all items of all
+// heads) at the rate the uniform split assumes.  `shape` gives kind, nitems,
+// total, causal, rows, keys and group.
+pdy::Split balanced_split(pdy::Split shape, int p, int64_t heads, double unit_us,
+                          double slice_bytes) {
+  if ((int64_t)p * shape.nitems * heads > kCUs) return uniform_split(p);
+  const int umax = shape.units(0);  // item 0 is the heaviest
+  int64_t total_units = 0;
+  for (int i = 0; i < shape.nitems; ++i) total_units += shape.units(i);
+  const double mean_load = (double)total_units * heads / kCUs;
+  auto entries = [&](int cap) {
+    int64_t n = 0;
+    for (int i = 0; i < shape.nitems; ++i) n += (shape.units(i) + cap - 1) / cap;
+    return n * heads;
+  };
+  auto cap_for = [&](int64_t budget) {
+    int lo = std::max(1, (umax + kMaxParts - 1) / kMaxParts), hi = umax;  // umax: one part each
+    while (lo < hi) {
+      const int mid = (lo + hi) / 2;
+      if (entries(mid) <= budget) hi = mid;
+      else lo = mid + 1;
+    }
+    return lo;
+  };
+  auto est_us = [&](int cap) {
+    const double parts_bytes = (double)entries(cap) * slice_bytes / ((double)shape.nitems * heads);
+    return std::max((double)cap, mean_load) * unit_us + 2.0 * parts_bytes / kPartBytesPerUs;
+  };
+  const int64_t b1 = (int64_t)p * shape.nitems * heads;
+  int cap = cap_for(b1);
+  if (b1 < kCUs) {
+    const int cap2 = cap_for(kCUs);
+    if (est_us(cap2) < est_us(cap)) cap = cap2;
+  }
+  shape.cap = cap;
+  shape.parts = (umax + cap - 1) / cap;
+  return shape.parts > 1 ? shape : uniform_split(1);
+}
+
+// workgroups per head of a launch of `items` items (per head) under split sp
+int64_t split_entries(const pdy::Split& sp, int64_t items) {
+  if (sp.cap == 0) return items * sp.parts;
+  int64_t n = 0;
+  for (int i = 0; i < sp.nitems; ++i) n += sp.nparts(i);
+  return n;
+}
+
+// The same split with about half the partial slices (for a fixed-size
+// workspace); parts = 1 when nothing is left to split.
+pdy::Split halve_split(pdy::Split sp) {
+  if (sp.cap == 0) return uniform_split(sp.parts / 2);
+  sp.cap *= 2;
+  sp.parts = (sp.units(0) + sp.cap - 1) / sp.cap;
+  return sp.parts > 1 ? sp : uniform_split(1);
+}
+
+// shape of a query-tile launch (forward, dQ) over a single segment
+pdy::Split q_shape(const Sizes& s, int causal, int rows, int keys) {
+  pdy::Split sp = uniform_split(1);
+  sp.kind = 0;
+  sp.nitems = tiles_of(s, rows);
+  sp.total = (int)s.T;
+  sp.causal = causal;
+  sp.rows = rows;
+  sp.keys = keys;
+  return sp;
+}
+
+// The split of a launch: none for context-parallel pairs (`chunk`), balanced
+// for causal single segments, else uniform.
+pdy::Split choose_split(int p, const Sizes& s, int causal, bool chunk, pdy::Split shape,
+                        int64_t heads, double unit_us, double slice_bytes) {
+  if (p <= 1 || chunk) return uniform_split(1);
+  if (s.N == 1 && causal) return balanced_split(shape, p, heads, unit_us, slice_bytes);
+  return uniform_split(p);
+}
+
+// sq: the query rows' sizes; sk: the keys' (the same for self-attention
+// over cu's segments, one chunk each for a context-parallel pair)
+pdy::Split fwd_split(const Sizes& sq, const Sizes& sk, int causal, bool chunk) {
+  const int rows = 32 * fwd_waves(sq), keys = fwd_key_tile(sq);
+  const double unit = tile_us((double)rows * keys, sq, 4.0, 4.5);
+  const double slice = (double)sq.T * sq.hq * sq.d * 4;
+  const int p = split_parts(grid_items(sq, rows) * sq.hq, tiles_of(sk, keys), unit, slice);
+  return choose_split(p, sq, causal, chunk, q_shape(sq, causal, rows, keys), sq.hq, unit, slice);
+}
+
+pdy::Split dq_split(const Sizes& sq, const Sizes& sk, int causal, bool chunk) {
   const int rows = 32 * fwd_waves(sq), keys = dq_key_tile(sq);
-  return split_parts(grid_items(sq, rows) * sq.hq, tiles_of(sk, keys),
-                     tile_us((double)rows * keys, sq, 6.0, 5.0),
-                     (double)sq.T * sq.hq * sq.d * 4);
+  const double unit = tile_us((double)rows * keys, sq, 6.0, 5.0);
+  const double slice = (double)sq.T * sq.hq * sq.d * 4;
+  const int p = split_parts(grid_items(sq, rows) * sq.hq, tiles_of(sk, keys), unit, slice);
+  return choose_split(p, sq, causal, chunk, q_shape(sq, causal, rows, keys), sq.hq, unit, slice);
 }
 
 // the heaviest key tile visits every 64-row query step of every head of its group
-int dkdv_split(const Sizes& sq, const Sizes& sk) {
+pdy::Split dkdv_split(const Sizes& sq, const Sizes& sk, int causal, bool chunk) {
   const int rows = pdy::DkdvCfg<128>::BQ;
-  return split_parts(grid_items(sk, kKvTile) * sk.hkv,
-                     (int64_t)tiles_of(sq, rows) * (sq.hq / sq.hkv),
-                     tile_us((double)rows * kKvTile, sq, 8.0, 4.5),
-                     2.0 * sk.T * sk.hkv * sk.d * 4);
+  const int g = (int)(sq.hq / sq.hkv);
+  const double unit = tile_us((double)rows * kKvTile, sq, 8.0, 4.5);
+  const double slice = 2.0 * sk.T * sk.hkv * sk.d * 4;
+  const int p = split_parts(grid_items(sk, kKvTile) * sk.hkv, (int64_t)tiles_of(sq, rows) * g,
+                            unit, slice);
+  pdy::Split shape = uniform_split(1);
+  shape.kind = 1;
+  shape.nitems = tiles_of(sk, kKvTile);
+  shape.total = (int)sk.T;
+  shape.causal = causal;
+  shape.rows = rows;
+  shape.keys = kKvTile;
+  shape.group = g;
+  return choose_split(p, sk, causal, chunk || sk.T == 0, shape, sk.hkv, unit, slice);
 }
 
 size_t part_o_bytes(const Sizes& s, int p) { return align256((size_t)p * s.T * s.hq * s.d * 4); }
@@ -235,21 +352,25 @@ size_t part_lse_bytes(const Sizes& s, int p) { return align256((size_t)p * s.hq 
 size_t part_kv_bytes(const Sizes& s, int p) { return align256((size_t)p * s.T * s.hkv * s.d * 4); }
 
 // workspace for a split forward's partial O and LSE (none if it is not split)
-size_t fwd_split_bytes(const Sizes& sq, const Sizes& sk) {
-  const int p = fwd_split(sq, sk);
-  return p > 1 ? part_o_bytes(sq, p) + part_lse_bytes(sq, p) : 0;
+size_t fwd_split_bytes(const pdy::Split& sp, const Sizes& sq) {
+  return sp.parts > 1 ? part_o_bytes(sq, sp.parts) + part_lse_bytes(sq, sp.parts) : 0;
 }
 
 // workspace for a split backward's partial dK, dV (key rows) and dQ
-size_t bwd_split_bytes(const Sizes& sq, const Sizes& sk) {
-  const int pk = sk.T > 0 ? dkdv_split(sq, sk) : 1, pq = dq_split(sq, sk);
-  return (pk > 1 ? 2 * part_kv_bytes(sk, pk) : 0) + (pq > 1 ? part_o_bytes(sq, pq) : 0);
+size_t bwd_split_bytes(const pdy::Split& kv, const pdy::Split& q, const Sizes& sq,
+                       const Sizes& sk) {
+  return (kv.parts > 1 ? 2 * part_kv_bytes(sk, kv.parts) : 0) +
+         (q.parts > 1 ? part_o_bytes(sq, q.parts) : 0);
 }
 
-// workspace of a (non-chunk) backward: both tile schedules, D and any split-K partials
+// workspace of a (non-chunk) backward, causal or not: both tile schedules, D
+// and any split-K partials
 size_t bwd_workspace_bytes(const Sizes& s) {
-  return plan_bytes(s, kKvTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) +
-         bwd_split_bytes(s, s);
+  size_t parts = 0;
+  for (int causal = 0; causal <= 1; ++causal)
+    parts = std::max(parts, bwd_split_bytes(dkdv_split(s, s, causal, false),
+                                            dq_split(s, s, causal, false), s, s));
+  return plan_bytes(s, kKvTile) + plan_bytes(s, 32 * fwd_waves(s)) + dd_bytes(s) + parts;
 }
 
 // A single segment (N = 1: by the contract cu = [0, T], and max_seqlen = T)
@@ -373,7 +494,9 @@ size_t attn_fwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq,
                                int32_t d) {
   Sizes s;
   if (check_sizes(T, N, maxlen, hq, hkv, d, &s) != PDY_OK) return 0;
-  return plan_bytes(s, 32 * fwd_waves(s)) + fwd_split_bytes(s, s);
+  return plan_bytes(s, 32 * fwd_waves(s)) +
+         std::max(fwd_split_bytes(fwd_split(s, s, 0, false), s),
+                  fwd_split_bytes(fwd_split(s, s, 1, false), s));
 }
 
 size_t attn_bwd_workspace_size(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv,
@@ -407,8 +530,9 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
   // a context-parallel pair does not split: the ring already overlaps its
   // forward calls on two streams, and the backward's partial traffic and
   // extra launches cancel the gain (measured at 131,072 tokens over p = 8)
-  const int nsplit = c.on ? 1 : fwd_split(s, sk);
-  const size_t need = plan_bytes(s, tile) + (nsplit > 1 ? fwd_split_bytes(s, sk) : 0);
+  const pdy::Split split = fwd_split(s, sk, causal, c.on);
+  const int nsplit = split.parts;
+  const size_t need = plan_bytes(s, tile) + fwd_split_bytes(split, s);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -435,7 +559,7 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
   a.chunked = c.on;
   a.tk = c.tk;
   a.shift = c.shift;
-  a.nsplit = nsplit;
+  a.split = split;
   a.part_o = nullptr;
   a.part_lse = nullptr;
   if (nsplit > 1) {
@@ -443,7 +567,7 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
     a.part_o = reinterpret_cast<float*>(w);
     a.part_lse = reinterpret_cast<float*>(w + part_o_bytes(s, nsplit));
   }
-  const dim3 grid((unsigned)(grid_items(s, tile) * s.hq * nsplit));
+  const dim3 grid((unsigned)(split_entries(split, grid_items(s, tile)) * s.hq));
   e = launch_timed(K_FWD, hs, [&] {
     if (s.d == 64) {
       if (nw == 8) launch_fwd<64, 8>(grid, hs, a);
@@ -461,10 +585,10 @@ pdy_status fwd_impl(const void* q, const void* k, const void* v, const int32_t* 
       uint16_t* out = static_cast<uint16_t*>(o);
       if (s.d == 64)
         hipLaunchKernelGGL(pdy::split_merge_kernel<64>, blocks, dim3(256), 0, hs, a.part_o,
-                           a.part_lse, nsplit, out, lse, (int)s.T, (int)s.hq);
+                           a.part_lse, split, out, lse, (int)s.T, (int)s.hq);
       else
         hipLaunchKernelGGL(pdy::split_merge_kernel<128>, blocks, dim3(256), 0, hs, a.part_o,
-                           a.part_lse, nsplit, out, lse, (int)s.T, (int)s.hq);
+                           a.part_lse, split, out, lse, (int)s.T, (int)s.hq);
     });
     if (e != hipSuccess) return hip_fail(e, "split_merge_kernel launch");
   }
@@ -485,22 +609,20 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   const int nwq = fwd_waves(s);
   const int qtile = 32 * nwq;
   // (no split-K for a context-parallel pair, as in the forward)
-  int nsplit_kv = c.on || sk.T == 0 ? 1 : dkdv_split(s, sk);
-  int nsplit_q = c.on ? 1 : dq_split(s, sk);
-  auto need_for = [&](int pk, int pq) {
-    return bwd_need(s, sk) + (pk > 1 ? 2 * part_kv_bytes(sk, pk) : 0) +
-           (pq > 1 ? part_o_bytes(s, pq) : 0);
-  };
+  pdy::Split split_kv = dkdv_split(s, sk, causal, c.on);
+  pdy::Split split_q = dq_split(s, sk, causal, c.on);
   // fit_splits: a fixed-size workspace takes fewer split-K parts (the larger
   // partial buffer halved first) when the chosen ones do not fit
-  while (fit_splits && need_for(nsplit_kv, nsplit_q) > workspace_bytes &&
-         (nsplit_kv > 1 || nsplit_q > 1)) {
-    const size_t bk = nsplit_kv > 1 ? 2 * part_kv_bytes(sk, nsplit_kv) : 0;
-    const size_t bq = nsplit_q > 1 ? part_o_bytes(s, nsplit_q) : 0;
-    if (bq >= bk) nsplit_q = nsplit_q == 2 ? 1 : nsplit_q / 2;
-    else nsplit_kv = nsplit_kv == 2 ? 1 : nsplit_kv / 2;
+  while (fit_splits && bwd_need(s, sk) + bwd_split_bytes(split_kv, split_q, s, sk) >
+                           workspace_bytes &&
+         (split_kv.parts > 1 || split_q.parts > 1)) {
+    const size_t bk = split_kv.parts > 1 ? 2 * part_kv_bytes(sk, split_kv.parts) : 0;
+    const size_t bq = split_q.parts > 1 ? part_o_bytes(s, split_q.parts) : 0;
+    if (bq >= bk) split_q = halve_split(split_q);
+    else split_kv = halve_split(split_kv);
   }
-  const size_t need = need_for(nsplit_kv, nsplit_q);
+  const int nsplit_kv = split_kv.parts, nsplit_q = split_q.parts;
+  const size_t need = bwd_need(s, sk) + bwd_split_bytes(split_kv, split_q, s, sk);
   if (workspace_bytes < need)
     return fail(PDY_ERR_WORKSPACE, "workspace has %zu bytes, %s needs %zu", workspace_bytes, who,
                 need);
@@ -560,8 +682,8 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   a.tk = c.tk;
   a.shift = c.shift;
   a.accumulate = c.accumulate;
-  a.nsplit_kv = nsplit_kv;
-  a.nsplit_q = nsplit_q;
+  a.split_kv = split_kv;
+  a.split_q = split_q;
   a.part_dk = a.part_dv = a.part_dq = nullptr;
   {
     uint8_t* w = reinterpret_cast<uint8_t*>(workspace) + bwd_need(s, sk);
@@ -574,16 +696,16 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   }
   // the parts' partial gradients, summed into dst (and parts_b into dst_b)
   auto sum_parts = [&](const float* parts, float* dst, const float* parts_b, float* dst_b,
-                       int nsplit, size_t n) {
+                       const pdy::Split& sp, size_t n, int row_elems) {
     const size_t threads = (parts_b ? 2 : 1) * (n / 4);
     const dim3 blocks((unsigned)((threads + 255) / 256));
     return launch_timed(K_SPLIT_SUM, hs, [&] {
       hipLaunchKernelGGL(pdy::split_sum_kernel, blocks, dim3(256), 0, hs, parts, dst, parts_b,
-                         dst_b, nsplit, n, c.accumulate);
+                         dst_b, sp, n, row_elems, c.accumulate);
     });
   };
   if (sk.T > 0) {
-    const dim3 gkv((unsigned)(grid_items(sk, kKvTile) * s.hkv * nsplit_kv));
+    const dim3 gkv((unsigned)(split_entries(split_kv, grid_items(sk, kKvTile)) * s.hkv));
     e = launch_timed(K_DKDV, hs, [&] {
       if (s.d == 64)
         hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
@@ -595,11 +717,12 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
     if (nsplit_kv > 1) {
       const size_t n = (size_t)sk.T * s.hkv * s.d;
-      if ((e = sum_parts(a.part_dk, dk, a.part_dv, dv, nsplit_kv, n)) != hipSuccess)
+      if ((e = sum_parts(a.part_dk, dk, a.part_dv, dv, split_kv, n, (int)(s.hkv * s.d))) !=
+          hipSuccess)
         return hip_fail(e, "split_sum_kernel launch");
     }
   }
-  const dim3 gq((unsigned)(grid_items(s, qtile) * s.hq * nsplit_q));
+  const dim3 gq((unsigned)(split_entries(split_q, grid_items(s, qtile)) * s.hq));
   e = launch_timed(K_DQ, hs, [&] {
     if (s.d == 64) {
       if (nwq == 8) launch_dq<64, 8>(gq, hs, a);
@@ -611,8 +734,8 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
   });
   if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
   if (nsplit_q > 1 &&
-      (e = sum_parts(a.part_dq, dq, nullptr, nullptr, nsplit_q, (size_t)s.T * s.hq * s.d)) !=
-          hipSuccess)
+      (e = sum_parts(a.part_dq, dq, nullptr, nullptr, split_q, (size_t)s.T * s.hq * s.d,
+                     (int)(s.hq * s.d))) != hipSuccess)
     return hip_fail(e, "split_sum_kernel launch");
   return PDY_OK;
 }

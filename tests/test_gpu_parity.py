@@ -219,6 +219,29 @@ def test_split_k(lengths, hq, hkv, d, expect):
                     expect_split=expect)
 
 
+# Causal single sequences too short to fill the chip take the balanced
+# split when its workgroups fit one round on the chip: the heaviest items (the
+# last query tiles, the first key tiles) are cut into more parts than light
+# ones.  Every element against the oracle; the combining launches show that
+# the split ran.
+@pytest.mark.parametrize("lengths,hq,hkv,d,expect", [
+    ([1024], 4, 4, 128, {"merge": 1, "sum": 2}),
+    ([2048], 4, 4, 128, {"merge": 1, "sum": 2}),
+    ([4096], 4, 4, 128, {"merge": 1, "sum": 2}),
+    ([3000], 8, 2, 128, {"merge": 1, "sum": 2}),   # ragged tail, grouped heads (dK/dV balanced)
+    ([1500], 2, 1, 64, {"merge": 1, "sum": 2}),    # d = 64
+    ([2048], 32, 8, 128, {"merge": 0, "sum": 2}),  # dK/dV balanced, dQ uniform, forward whole
+])
+def test_balanced_split_full_parity(lengths, hq, hkv, d, expect):
+    from paper_2511_13198_amd import pdyattn
+    pdyattn.profile_start()
+    _full_parity(lengths, hq, hkv, d, True)
+    prof = pdyattn.profile_stop()
+    got = {"merge": prof.get("split_merge_kernel", (0, 0.0))[0],
+           "sum": prof.get("split_sum_kernel", (0, 0.0))[0]}
+    assert got == expect, f"split-K launches {got}, expected {expect}"
+
+
 @pytest.mark.parametrize("nseg,hi,hq,hkv,d", [
     (16384, 64, 2, 1, 64),    # every segment <= 128 tokens: the 4-wave kernels
     (6000, 300, 4, 2, 128),   # 8-wave kernels
