@@ -3,18 +3,20 @@
 // P = exp(S - LSE), D_i = <dO_i, O_i>:
 //   dV = P^T dO,  dP = dO V^T,  dS = P * (dP - D),  dK = scale * dS^T Q,
 //   dQ = scale * dS K.
-// Three kernels:
-//   * bwd_pre_kernel    D = rowsum(dO * O) (fp32, [Hq, T]) -- bandwidth bound.
+// Two kernels, in this order:
+//   * bwd_dq_kernel     one workgroup per (segment, query head, 32-row-per-wave
+//                       tile); mirrors the forward: computes its rows'
+//                       D = rowsum(dO * O) (fp32, written to [Hq, T] for the
+//                       next kernel), recomputes S^T and dP^T, forms dS^T and
+//                       accumulates dQ^T = K^T dS^T.  No atomics.
 //   * bwd_dkdv_kernel   one workgroup per (segment, kv head, 256-key tile); a
 //                       wave owns 32 keys (K in an LDS tile, V in registers),
 //                       keeps their dK^T / dV^T in accumulators, and sweeps
 //                       every query head of the group and every 64-row query
 //                       step that sees the keys.  Written once, no atomics.
-//   * bwd_dq_kernel     one workgroup per (segment, query head, 32-row-per-wave
-//                       tile); mirrors the forward: recomputes S^T and dP^T,
-//                       forms dS^T and accumulates dQ^T = K^T dS^T.  No atomics.
 // When a launch cannot fill the chip, a workgroup takes one part of a tile's
-// work (split-K) and split_sum_kernel adds the parts' partial gradients.
+// work (split-K) and one split_sum_kernel launch adds the parts' partial
+// gradients of both.
 // All outputs are deterministic.
 #pragma once
 #include "common.hpp"
@@ -22,62 +24,44 @@
 
 namespace pdy {
 
-// dst = (accumulate ? dst : 0) + sum_p parts[p * n + i] over the partial
-// gradients of a split-K backward, in part order, for one array
-// (parts_b == nullptr) or two of the same size (dK and dV in one launch:
-// the grid's second half takes the second); 4 floats per thread (n is a
-// multiple of 4: a head dimension of 64 or 128 divides it).  Element i
-// belongs to query row or key i / row_elems, which has sp.nparts of its
-// item.
-__global__ void __launch_bounds__(256) split_sum_kernel(const float* __restrict__ parts_a,
-                                                        float* __restrict__ dst_a,
-                                                        const float* __restrict__ parts_b,
-                                                        float* __restrict__ dst_b, Split sp,
-                                                        size_t n, int row_elems, int accumulate) {
-  size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  const float* parts = parts_a;
-  float* dst = dst_a;
-  if (i >= n) {
-    if (parts_b == nullptr) return;
-    i -= n;
-    if (i >= n) return;
-    parts = parts_b;
-    dst = dst_b;
-  }
-  const int nsplit = sp.nparts(sp.item_of((int)(i / row_elems)));
-  f32x4 acc = accumulate ? *reinterpret_cast<const f32x4*>(dst + i) : f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int p = 0; p < nsplit; ++p) acc += *reinterpret_cast<const f32x4*>(parts + p * n + i);
-  *reinterpret_cast<f32x4*>(dst + i) = acc;
+// One array of split-K partial gradients to sum: dst = (accumulate ? dst :
+// 0) + sum_p parts[p * n + i] in part order, where element i belongs to
+// query row or key i / row_elems, which has sp.nparts of its item.  A split
+// launch has fewer than 512 items of at most 256 rows or keys, so n < 2^31.
+struct SumJob {
+  const float* parts;  // [sp.parts][n]
+  float* dst;          // [n]
+  uint32_t n;          // floats (a multiple of 4: a head dimension of 64 or 128 divides it)
+  int row_elems;       // floats per query row or key
+  Split sp;
+};
+struct SumJobs {
+  SumJob job[3];
+  int blocks[3];  // workgroups of each job, one after another in the grid
+  int njobs;
+  int accumulate;
+};
+
+__device__ __forceinline__ void sum_job(const SumJob& b, int block, int accumulate) {
+  const uint32_t i = ((uint32_t)block * 256u + threadIdx.x) * 4u;
+  if (i >= b.n) return;
+  const int nsplit = b.sp.nparts(b.sp.item_of((int)(i / (uint32_t)b.row_elems)));
+  f32x4 acc = accumulate ? *reinterpret_cast<const f32x4*>(b.dst + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < nsplit; ++p)
+    acc += *reinterpret_cast<const f32x4*>(b.parts + (size_t)p * b.n + i);
+  *reinterpret_cast<f32x4*>(b.dst + i) = acc;
 }
 
-// D[h][i] = sum_d dO[i,h,d] * O[i,h,d]; one 16-lane group per (row, head).
-template <int D>
-__global__ void __launch_bounds__(256) bwd_pre_kernel(const uint16_t* __restrict__ o,
-                                                      const uint16_t* __restrict__ dout,
-                                                      float* __restrict__ dd, int total_tokens,
-                                                      int hq) {
-  constexpr int LANES = D / 8;  // 16 B per lane
-  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t pair = gid / LANES;  // (row, head) flattened as row * hq + h
-  const int sub = (int)(gid % LANES);
-  const size_t npairs = (size_t)total_tokens * hq;
-  float acc = 0.f;
-  if (pair < npairs) {
-    const u32x4 ov = *reinterpret_cast<const u32x4*>(o + pair * D + sub * 8);
-    const u32x4 gv = *reinterpret_cast<const u32x4*>(dout + pair * D + sub * 8);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      acc += __uint_as_float(ov[i] << 16) * __uint_as_float(gv[i] << 16);
-      acc += __uint_as_float(ov[i] & 0xffff0000u) * __uint_as_float(gv[i] & 0xffff0000u);
-    }
-  }
-#pragma unroll
-  for (int off = LANES / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, LANES);
-  if (pair < npairs && sub == 0) {
-    const size_t row = pair / hq;
-    const int h = (int)(pair % hq);
-    dd[(size_t)h * total_tokens + row] = acc;
-  }
+// The partial sums of a split-K backward (dQ, and dK and dV) in one launch:
+// 4 floats per thread; each workgroup belongs to one job (so the job's
+// fields are uniform over it).
+__global__ void __launch_bounds__(256) split_sum_kernel(SumJobs jobs) {
+  int b = blockIdx.x;
+  if (b < jobs.blocks[0]) return sum_job(jobs.job[0], b, jobs.accumulate);
+  b -= jobs.blocks[0];
+  if (jobs.njobs > 1 && b < jobs.blocks[1]) return sum_job(jobs.job[1], b, jobs.accumulate);
+  b -= jobs.blocks[1];
+  if (jobs.njobs > 2 && b < jobs.blocks[2]) sum_job(jobs.job[2], b, jobs.accumulate);
 }
 
 #ifndef PDY_DQ_BK
@@ -91,9 +75,10 @@ struct BwdArgs {
   const uint16_t* q;
   const uint16_t* k;
   const uint16_t* v;
+  const uint16_t* o;
   const uint16_t* dout;
   const float* lse;  // natural log, [Hq, T]
-  const float* dd;   // [Hq, T]
+  float* dd;         // D = rowsum(dO * O), [Hq, T]: written by the dQ kernel, read by dK/dV
   const int32_t* cu;
   float* dq;
   float* dk;
@@ -503,22 +488,31 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const size_t qstride = (size_t)a.hq * D;
   const size_t kvstride = (size_t)a.hkv * D;
 
+  // Q and dO of the lane's row as B operands; D = <dO, O> of the row from
+  // the lane's half of its elements and the partner lane's (l ^ 32)
   bf16x8 qf[D / 16], gf[D / 16];
   float lse2 = 0.f, ddv = 0.f;
   {
     const bool ok = row < seg_hi;
-    const uint16_t* qp = a.q + (size_t)row * qstride + (size_t)h * D + hh * 8;
-    const uint16_t* gp = a.dout + (size_t)row * qstride + (size_t)h * D + hh * 8;
+    const size_t roff = (size_t)row * qstride + (size_t)h * D + hh * 8;
+    float dsum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      qf[ks] = load_bf16x8(qp + ks * 16, ok);
-      gf[ks] = load_bf16x8(gp + ks * 16, ok);
+      qf[ks] = load_bf16x8(a.q + roff + ks * 16, ok);
+      gf[ks] = load_bf16x8(a.dout + roff + ks * 16, ok);
+      const bf16x8 of = load_bf16x8(a.o + roff + ks * 16, ok);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        dsum[j & 3] = __builtin_fmaf((float)of[j], (float)gf[ks][j], dsum[j & 3]);
     }
+    ddv = (dsum[0] + dsum[1]) + (dsum[2] + dsum[3]);
+    ddv += partner32(ddv);
     if (ok) {
       lse2 = a.lse[(size_t)h * a.total_tokens + row] * kLog2e;
-      ddv = a.dd[(size_t)h * a.total_tokens + row];
       // a row without any visible key has LSE = -inf and no gradient
       if (lse2 == -INFINITY) lse2 = INFINITY;
+      // D of the row for the dK/dV kernel, which runs after this one
+      if (hh == 0 && part == 0) a.dd[(size_t)h * a.total_tokens + row] = ddv;
     }
   }
   f32x16 dqa[D / 32];

@@ -98,11 +98,10 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Optional per-thread kernel timing: while enabled, every launch is bracketed
 // by two events on its own stream; pdy_profile_stop reduces them per kernel.
 // ---------------------------------------------------------------------------
-enum KernelId { K_PLAN = 0, K_FWD, K_PRE, K_DKDV, K_DQ, K_SPLIT_MERGE, K_SPLIT_SUM, K_COUNT };
-const char* const kKernelNames[K_COUNT] = {"plan_kernel",        "fwd_kernel",
-                                           "bwd_pre_kernel",     "bwd_dkdv_kernel",
-                                           "bwd_dq_kernel",      "split_merge_kernel",
-                                           "split_sum_kernel"};
+enum KernelId { K_PLAN = 0, K_FWD, K_DKDV, K_DQ, K_SPLIT_MERGE, K_SPLIT_SUM, K_COUNT };
+const char* const kKernelNames[K_COUNT] = {"plan_kernel",     "fwd_kernel",
+                                           "bwd_dkdv_kernel", "bwd_dq_kernel",
+                                           "split_merge_kernel", "split_sum_kernel"};
 struct ProfRec {
   int kid;
   hipEvent_t a, b;
@@ -305,7 +304,9 @@ pdy::Split q_shape(const Sizes& s, int causal, int rows, int keys) {
 // for causal single segments, else uniform.
 pdy::Split choose_split(int p, const Sizes& s, int causal, bool chunk, pdy::Split shape,
                         int64_t heads, double unit_us, double slice_bytes) {
-  if (p <= 1 || chunk) return uniform_split(1);
+  // (a split launch has fewer than 512 items, so a slice holds far fewer than
+  // the 2^31 floats the combine kernels index with 32 bits; kept as a guard)
+  if (p <= 1 || chunk || slice_bytes / 4 >= 2147483648.0) return uniform_split(1);
   if (s.N == 1 && causal) return balanced_split(shape, p, heads, unit_us, slice_bytes);
   return uniform_split(p);
 }
@@ -644,25 +645,11 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
         (st = launch_plans(q_job, sk.T > 0 ? &kv_job : nullptr, hs)) != PDY_OK)
       return st;
   }
-  {
-    const size_t threads = (size_t)s.T * s.hq * (s.d / 8);
-    const unsigned blocks = (unsigned)((threads + 255) / 256);
-    e = launch_timed(K_PRE, hs, [&] {
-      if (s.d == 64)
-        hipLaunchKernelGGL(pdy::bwd_pre_kernel<64>, dim3(blocks), dim3(256), 0, hs,
-                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
-                           (int)s.T, (int)s.hq);
-      else
-        hipLaunchKernelGGL(pdy::bwd_pre_kernel<128>, dim3(blocks), dim3(256), 0, hs,
-                           static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(dout), dd,
-                           (int)s.T, (int)s.hq);
-    });
-    if (e != hipSuccess) return hip_fail(e, "bwd_pre_kernel launch");
-  }
   pdy::BwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
   a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<const uint16_t*>(o);
   a.dout = static_cast<const uint16_t*>(dout);
   a.lse = lse;
   a.dd = dd;
@@ -694,34 +681,7 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     }
     if (nsplit_q > 1) a.part_dq = reinterpret_cast<float*>(w);
   }
-  // the parts' partial gradients, summed into dst (and parts_b into dst_b)
-  auto sum_parts = [&](const float* parts, float* dst, const float* parts_b, float* dst_b,
-                       const pdy::Split& sp, size_t n, int row_elems) {
-    const size_t threads = (parts_b ? 2 : 1) * (n / 4);
-    const dim3 blocks((unsigned)((threads + 255) / 256));
-    return launch_timed(K_SPLIT_SUM, hs, [&] {
-      hipLaunchKernelGGL(pdy::split_sum_kernel, blocks, dim3(256), 0, hs, parts, dst, parts_b,
-                         dst_b, sp, n, row_elems, c.accumulate);
-    });
-  };
-  if (sk.T > 0) {
-    const dim3 gkv((unsigned)(split_entries(split_kv, grid_items(sk, kKvTile)) * s.hkv));
-    e = launch_timed(K_DKDV, hs, [&] {
-      if (s.d == 64)
-        hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
-                           pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
-      else
-        hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
-                           pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
-    });
-    if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
-    if (nsplit_kv > 1) {
-      const size_t n = (size_t)sk.T * s.hkv * s.d;
-      if ((e = sum_parts(a.part_dk, dk, a.part_dv, dv, split_kv, n, (int)(s.hkv * s.d))) !=
-          hipSuccess)
-        return hip_fail(e, "split_sum_kernel launch");
-    }
-  }
+  // dQ first: it also writes D = rowsum(dO * O), which dK/dV reads
   const dim3 gq((unsigned)(split_entries(split_q, grid_items(s, qtile)) * s.hq));
   e = launch_timed(K_DQ, hs, [&] {
     if (s.d == 64) {
@@ -733,10 +693,43 @@ pdy_status bwd_impl(const void* q, const void* k, const void* v, const void* o, 
     }
   });
   if (e != hipSuccess) return hip_fail(e, "bwd_dq_kernel launch");
-  if (nsplit_q > 1 &&
-      (e = sum_parts(a.part_dq, dq, nullptr, nullptr, split_q, (size_t)s.T * s.hq * s.d,
-                     (int)(s.hq * s.d))) != hipSuccess)
-    return hip_fail(e, "split_sum_kernel launch");
+  if (sk.T > 0) {
+    const dim3 gkv((unsigned)(split_entries(split_kv, grid_items(sk, kKvTile)) * s.hkv));
+    e = launch_timed(K_DKDV, hs, [&] {
+      if (s.d == 64)
+        hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<64>, gkv, dim3(pdy::DkdvCfg<64>::NT),
+                           pdy::DkdvCfg<64>::LDS_BYTES, hs, a);
+      else
+        hipLaunchKernelGGL(pdy::bwd_dkdv_kernel<128>, gkv, dim3(pdy::DkdvCfg<128>::NT),
+                           pdy::DkdvCfg<128>::LDS_BYTES, hs, a);
+    });
+    if (e != hipSuccess) return hip_fail(e, "bwd_dkdv_kernel launch");
+  }
+  // the parts' partial gradients (dQ, dK, dV), summed in one launch
+  pdy::SumJobs jobs{};
+  jobs.njobs = 0;
+  jobs.accumulate = c.accumulate;
+  int64_t sum_blocks = 0;
+  auto add_job = [&](const float* parts, float* dst, size_t n, int row_elems,
+                     const pdy::Split& sp) {
+    const int blocks = (int)((n / 4 + 255) / 256);
+    jobs.blocks[jobs.njobs] = blocks;
+    jobs.job[jobs.njobs++] = pdy::SumJob{parts, dst, (uint32_t)n, row_elems, sp};
+    sum_blocks += blocks;
+  };
+  if (nsplit_q > 1) add_job(a.part_dq, dq, (size_t)s.T * s.hq * s.d, (int)(s.hq * s.d), split_q);
+  if (sk.T > 0 && nsplit_kv > 1) {
+    const size_t n = (size_t)sk.T * s.hkv * s.d;
+    add_job(a.part_dk, dk, n, (int)(s.hkv * s.d), split_kv);
+    add_job(a.part_dv, dv, n, (int)(s.hkv * s.d), split_kv);
+  }
+  if (jobs.njobs > 0) {
+    const dim3 blocks((unsigned)sum_blocks);
+    e = launch_timed(K_SPLIT_SUM, hs, [&] {
+      hipLaunchKernelGGL(pdy::split_sum_kernel, blocks, dim3(256), 0, hs, jobs);
+    });
+    if (e != hipSuccess) return hip_fail(e, "split_sum_kernel launch");
+  }
   return PDY_OK;
 }
 

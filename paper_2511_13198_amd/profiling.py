@@ -32,8 +32,8 @@ import re
 from typing import Dict, List
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIBRARY_KERNELS = ("plan_kernel", "fwd_kernel", "bwd_pre_kernel", "bwd_dkdv_kernel",
-                   "bwd_dq_kernel", "split_merge_kernel", "split_sum_kernel")
+LIBRARY_KERNELS = ("plan_kernel", "fwd_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel",
+                   "split_merge_kernel", "split_sum_kernel")
 
 
 def code_text(src: str) -> str:
