@@ -15,6 +15,9 @@ CASES = [
     # (lengths, Hq, Hkv, d, same_path): the first splits its work into parts
     # whose partial gradients exceed the 64 MiB scratch, so it runs with fewer
     ([3000, 5000, 77], 4, 2, 128, False),
+    # a causal single sequence: a balanced split whose partials exceed the
+    # scratch, so its parts are halved (larger units per part)
+    ([4096], 4, 4, 128, False),
     ([16384], 8, 8, 64, True),          # fills the chip: no split
     ([700, 1, 129], 2, 1, 64, True),    # split parts that fit
 ]
