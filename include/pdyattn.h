@@ -37,9 +37,12 @@
  *     error text and the optional per-thread kernel timing records.
  *   - Results are bitwise reproducible run to run (no atomics feed outputs).
  *   - Launches too small to fill the GPU (fewer than 512 work items, e.g. a
- *     single 8K-token sequence over 4 heads) split each item's work into 2 or
- *     4 parts (split-K) whose fp32 partial results are combined in a second
- *     kernel; the choice depends only on the sizes.  A segment's results
+ *     single 8K-token sequence over 4 heads) split each item's work into
+ *     parts (split-K) whose fp32 partial results are combined in a second
+ *     kernel: 2 or 4 parts per item, or, for a causal single sequence whose
+ *     parts fit one round on the GPU, more parts for the heavier items (at
+ *     most 16); the choice depends only on the sizes and the causal flag
+ *     (the workspace queries cover both values of the flag).  A segment's results
  *     therefore do not depend on the other segments of its batch, but a batch
  *     and the same segment alone may round differently when one of the two
  *     launches is split.
@@ -63,14 +66,14 @@ typedef enum {
 } pdy_status;
 
 /* Bytes of workspace attn_fwd needs for these sizes (>= 256; for a split-K
- * launch it includes the parts' fp32 O and LSE, about 128 MiB at most).
+ * launch it includes the parts' fp32 O and LSE, under 128 MiB).
  * Returns 0 when the sizes are invalid. */
 size_t attn_fwd_workspace_size(int32_t total_tokens, int32_t num_seqs, int32_t max_seqlen,
                                int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim);
 
 /* Bytes of workspace attn_bwd needs (it holds D = rowsum(dO * O), fp32
  * [Hq, T], the tile schedules and, for split-K launches, the parts' fp32
- * partial gradients, about 256 MiB at most).  Returns 0 when the sizes are
+ * partial gradients, under 384 MiB).  Returns 0 when the sizes are
  * invalid. */
 size_t attn_bwd_workspace_size(int32_t total_tokens, int32_t num_seqs, int32_t max_seqlen,
                                int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim);

@@ -165,9 +165,10 @@ int64_t grid_items(const Sizes& s, int tile) {
 // is taken only while that saves time by the estimate below: a tile's time
 // from the kernels' measured throughput per CU (≈ 4.5 TFLOP/s forward and
 // dK/dV, ≈ 5 dQ), the partial traffic at ≈ 4 TB/s, plus one launch.  The
-// decision depends on the sizes alone, so the workspace queries reproduce
-// it; partial buffers exist only for launches this small (parts x items <
-// 2 kFillItems: at most 1024 x 256 rows of partial results).
+// decision depends on the sizes alone (balanced_split below also on the
+// causal flag), so the workspace queries reproduce it; partial buffers exist
+// only for launches this small (parts x items < 2 kFillItems, or at most
+// kMaxParts slices of a balanced split of fewer than kCUs workgroups).
 constexpr int64_t kFillItems = 512;
 constexpr int kMaxSplit = 4;
 constexpr double kPartBytesPerUs = 4.0e6;  // partial results written + read back
