@@ -52,6 +52,8 @@ def _full_parity(lengths, hq, hkv, d, causal, scale=None, seed=wl.SEED):
     ([1], 1, 1, 64, True, None),                            # single token
     ([128, 1, 100, 37, 128], 4, 2, 128, True, None),        # every segment <= 128: 4-wave kernels
     ([96, 3, 128], 2, 2, 128, False, None),                 # same, non-causal
+    ([700, 1300, 45], 6, 2, 128, True, None),               # three query heads per kv head
+    ([900, 257], 3, 3, 64, False, None),                    # odd head count, non-causal
 ])
 def test_full_parity_small(lengths, hq, hkv, d, causal, scale):
     _full_parity(lengths, hq, hkv, d, causal, scale)
@@ -231,6 +233,7 @@ def test_split_k(lengths, hq, hkv, d, expect):
     ([3000], 8, 2, 128, {"merge": 1, "sum": 1}),   # ragged tail, grouped heads (dK/dV balanced)
     ([1500], 2, 1, 64, {"merge": 1, "sum": 1}),    # d = 64
     ([2048], 32, 8, 128, {"merge": 0, "sum": 1}),  # dK/dV balanced, dQ uniform, forward whole
+    ([2500], 6, 2, 128, {"merge": 1, "sum": 1}),   # three query heads per kv head
 ])
 def test_balanced_split_full_parity(lengths, hq, hkv, d, expect):
     from paper_2511_13198_amd import pdyattn
