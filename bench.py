@@ -51,7 +51,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the sequence-length sweep timed after the main line")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=12288,
+    ap.add_argument("--cpu-sample-tokens", type=int, default=40960,
                     help="causal prefix length the CPU oracle is timed on")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times), for "
