@@ -48,11 +48,16 @@ int tiles_of(const Sizes& s, int tile) {
   return n < 1 ? 1 : (int)n;
 }
 
-// forward workgroup size: 8 waves (256 query rows) unless segments are short
+// forward and dQ workgroup size: 8 waves (256 query rows, 128-key tiles, one
+// workgroup per CU) unless every segment has at most kShortSeg tokens; then
+// 4 waves (128 rows, 64-key tiles, two workgroups per CU), whose smaller
+// items and diagonal tiles outweigh their extra barriers there (measured
+// fwd+bwd: 1K-2K tokens 7-12 % faster, 4K and longer 3-15 % slower)
 #ifndef PDY_WAVES_LONG
 #define PDY_WAVES_LONG 8
 #endif
-int fwd_waves(const Sizes& s) { return s.maxlen > 128 ? PDY_WAVES_LONG : 4; }
+constexpr int64_t kShortSeg = 2048;
+int fwd_waves(const Sizes& s) { return s.maxlen > kShortSeg ? PDY_WAVES_LONG : 4; }
 
 pdy_status check_sizes(int32_t T, int32_t N, int32_t maxlen, int32_t hq, int32_t hkv, int32_t d,
                        Sizes* out) {

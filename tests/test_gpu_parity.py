@@ -50,10 +50,12 @@ def _full_parity(lengths, hq, hkv, d, causal, scale=None, seed=wl.SEED):
     ([300, 65, 1], 4, 4, 128, False, None),
     ([2048, 33], 8, 2, 128, True, None),
     ([1], 1, 1, 64, True, None),                            # single token
-    ([128, 1, 100, 37, 128], 4, 2, 128, True, None),        # every segment <= 128: 4-wave kernels
+    ([128, 1, 100, 37, 128], 4, 2, 128, True, None),        # every segment <= 2048: 4-wave kernels
     ([96, 3, 128], 2, 2, 128, False, None),                 # same, non-causal
     ([700, 1300, 45], 6, 2, 128, True, None),               # three query heads per kv head
     ([900, 257], 3, 3, 64, False, None),                    # odd head count, non-causal
+    ([2100, 300, 1], 4, 2, 128, True, None),                # a segment > 2048: 8-wave kernels
+    ([2200], 2, 2, 64, False, None),                        # same, non-causal, d = 64
 ])
 def test_full_parity_small(lengths, hq, hkv, d, causal, scale):
     _full_parity(lengths, hq, hkv, d, causal, scale)
@@ -246,11 +248,12 @@ def test_balanced_split_full_parity(lengths, hq, hkv, d, expect):
 
 
 @pytest.mark.parametrize("nseg,hi,hq,hkv,d", [
-    (16384, 64, 2, 1, 64),    # every segment <= 128 tokens: the 4-wave kernels
-    (6000, 300, 4, 2, 128),   # 8-wave kernels
+    (16384, 64, 2, 1, 64),    # every segment <= 2048 tokens: the 4-wave kernels
+    (6000, 300, 4, 2, 128),   # same, d = 128
+    (1000, 3000, 2, 1, 128),  # segments up to 3000 tokens: the 8-wave kernels
 ])
 def test_many_segments(nseg, hi, hq, hkv, d):
-    """Batches of thousands of short segments (lengths uniform in 1..hi): the
+    """Batches of a thousand or more segments (lengths uniform in 1..hi): the
     tile schedule is a counting sort, far below a millisecond per launch, and
     sampled rows and the tail key columns of three segments match the oracle."""
     rng = np.random.default_rng(7)
