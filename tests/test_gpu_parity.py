@@ -61,6 +61,48 @@ def test_full_parity_small(lengths, hq, hkv, d, causal, scale):
     _full_parity(lengths, hq, hkv, d, causal, scale)
 
 
+@pytest.mark.parametrize("lengths,hq,hkv,d,causal", [
+    ([3000], 2, 1, 128, True),        # 8-wave forward
+    ([1500, 700], 2, 2, 64, True),    # 4-wave forward
+    ([2600], 2, 2, 128, False),       # non-causal
+    ([4096], 2, 2, 128, True),        # balanced split-K: every part sets its own offset
+])
+def test_forward_logits_rising_past_first_keys(lengths, hq, hkv, d, causal):
+    """Keys 512-1023 of each segment scaled by 64 and keys from 1024 on by
+    128 (exact in bf16): their logits rise 100-300 (natural units) above the
+    first keys' maximum, so the forward must raise its exponent offset both
+    where 2^(s c - m) overflows to inf and where it only grows large.  O and
+    LSE against the oracle; V is halved (exact) because such peaked rows put
+    O on single values of V, whose bf16 rounding alone would otherwise sit at
+    the absolute tolerance.  (The gradients of such rows scale with the key
+    norms, beyond the absolute tolerance, and take no part in this path.)"""
+    import torch
+    from paper_2511_13198_amd import pdyattn
+    scale = 1.0 / math.sqrt(d)
+    pu.log(f"  case lengths={lengths} Hq={hq} Hkv={hkv} d={d} causal={causal}")
+    bits, cu = _host_case(lengths, hq, hkv, d)
+    f = {n: wl.bf16_bits_to_f64(b) for n, b in bits.items()}
+    k = f["k"].copy()
+    for a, b in zip(cu[:-1], cu[1:]):
+        k[a + 512:min(b, a + 1024)] *= 64.0
+        k[a + 1024:b] *= 128.0
+    vh = f["v"] * 0.5
+    q = pu.to_device_bf16(bits["q"])
+    kd = torch.from_numpy(k).to(torch.bfloat16).cuda()
+    v = torch.from_numpy(vh).to(torch.bfloat16).cuda()
+    assert np.array_equal(kd.double().cpu().numpy(), k), "scaling by powers of two stays exact"
+    assert np.array_equal(v.double().cpu().numpy(), vh), "scaling by powers of two stays exact"
+    cu_d = torch.from_numpy(cu).cuda()
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((hq, q.shape[0]), float("nan"), dtype=torch.float32, device="cuda")
+    pdyattn.attn_fwd(q, kd, v, cu_d, max(lengths), causal, scale, out=o, lse=lse)
+    torch.cuda.synchronize()
+    ro, rlse = ora.forward(f["q"], k, vh, cu, causal, scale)
+    assert np.max(rlse) > 100.0, "the inputs reach the large-logit regime"
+    pu.check_close("O", pu.bf16_to_f64(o), ro)
+    pu.check_close("LSE", lse.cpu().numpy(), rlse)
+
+
 def _run_counted(dev, cu_d, max_seqlen, scale):
     """run_gpu, and whether any split-K combining kernel ran."""
     from paper_2511_13198_amd import pdyattn
