@@ -66,7 +66,7 @@ typedef enum {
 } pdy_status;
 
 /* Bytes of workspace attn_fwd needs for these sizes (>= 256; for a split-K
- * launch it includes the parts' fp32 O and LSE, under 128 MiB).
+ * launch it includes the parts' fp32 O and LSE, under 129 MiB).
  * Returns 0 when the sizes are invalid. */
 size_t attn_fwd_workspace_size(int32_t total_tokens, int32_t num_seqs, int32_t max_seqlen,
                                int32_t num_heads_q, int32_t num_heads_kv, int32_t head_dim);

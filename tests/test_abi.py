@@ -191,6 +191,22 @@ def test_bwd_chunk_argument_errors(kw, status, msg):
     assert msg in P.last_error()
 
 
+def test_workspace_bounds_over_a_size_sweep():
+    """The header's bounds on the split-K workspaces (forward under 129 MiB,
+    backward under 384 MiB) over single sequences and packed batches of the
+    sizes that split (the largest: two parts of a 130,816-token sequence)."""
+    worst_f = worst_b = 0
+    for d in (64, 128):
+        for hq, hkv in ((1, 1), (2, 1), (4, 4), (6, 2), (8, 2), (32, 8)):
+            for T in list(range(64, 8192, 448)) + list(range(8192, 131073, 4096)) + [130816]:
+                for n in (1, 3):
+                    maxlen = T if n == 1 else (T + n - 1) // n
+                    worst_f = max(worst_f, P.fwd_workspace_size(T, n, maxlen, hq, hkv, d))
+                    worst_b = max(worst_b, P.bwd_workspace_size(T, n, maxlen, hq, hkv, d))
+    assert 128 * MiB < worst_f < 129 * MiB
+    assert 383 * MiB < worst_b < 384 * MiB
+
+
 def test_chunk_noops_and_workspace_sizes():
     # no query rows: nothing to do (k and v may be absent)
     assert _fwd_chunk(tq=0, q=0, k=0, v=0, o=0, lse=0, ws=0, wsb=0) == P.PDY_OK
