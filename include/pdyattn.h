@@ -33,8 +33,10 @@
  *   - Scratch memory comes from the caller's `workspace` (16-byte aligned,
  *     at least the size the matching *_workspace_size query returns).
  *   - Calls on different streams with disjoint outputs and workspaces may run
- *     concurrently; the library holds no global state besides per-thread
- *     error text and the optional per-thread kernel timing records.
+ *     concurrently, except attn_bwd_noalloc calls on the same GPU (they share
+ *     its static scratch array); the library holds no other global state
+ *     besides per-thread error text, the optional per-thread kernel timing
+ *     records and a one-time setup of kernel attributes.
  *   - Results are bitwise reproducible run to run (no atomics feed outputs).
  *   - Launches too small to fill the GPU (fewer than 512 work items, e.g. a
  *     single 8K-token sequence over 4 heads) split each item's work into
