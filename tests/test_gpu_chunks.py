@@ -45,6 +45,9 @@ PAIRS = [
     (700, 2, 2, 64, True, (129, 700), (1, 257)),
     (600, 2, 1, 128, False, (0, 333), (100, 600)),
     (300, 2, 2, 128, True, (0, 300), (0, 0)),         # empty key chunk
+    # query chunks over 2,048 rows: the 8-wave kernels
+    (5000, 2, 1, 128, True, (2100, 5000), (1000, 3500)),
+    (4500, 2, 2, 64, False, (0, 2300), (2000, 4500)),
 ]
 
 
@@ -106,6 +109,7 @@ def test_chunks_merge_to_full_attention(T, hq, hkv, d, causal, cuts):
     (1200, 4, 2, 128, True, [0, 300, 700, 1200]),
     (800, 2, 2, 64, True, [0, 257, 800]),
     (600, 2, 1, 128, False, [0, 200, 600]),
+    (5000, 2, 1, 128, True, [0, 2200, 5000]),     # chunks over 2,048 rows: 8-wave kernels
 ])
 def test_chunk_gradients(T, hq, hkv, d, causal, cuts):
     """Each pair against the oracle's pair contribution, and the sums against

@@ -315,6 +315,15 @@ def test_single_65536_one_kv_head():
                     tail_cols=256, expect_split={"merge": 0, "sum": 1})
 
 
+def test_single_65536_head_dim_64():
+    """The d = 64 kernels on a long sequence (8 heads, 256 query tiles per
+    head: no split), sampled rows and tail keys against the oracle plus the
+    identities over every element."""
+    w = wl.Workload("single65536_h8_d64", [65536], 8, 8, 64)
+    _sampled_parity(w, device_gen=True, heads=[0, 7], kv_heads=[3], per_seg_random=48,
+                    tail_cols=256, expect_split={"merge": 0, "sum": 0})
+
+
 def test_plan_with_a_loose_length_bound():
     """max_seqlen only bounds the segment lengths: 1000 segments (about 800K
     tokens, one head) passed with max_seqlen = T give more tile counts than
