@@ -61,6 +61,34 @@ def test_full_parity_small(lengths, hq, hkv, d, causal, scale):
     _full_parity(lengths, hq, hkv, d, causal, scale)
 
 
+def _random_shapes(n=40, seed=2511):
+    """Seeded random small shapes: 1-4 segments of 0-3,000 tokens (some
+    empty), query/kv head groups of 1-4, d in {64, 128}, either causal flag
+    and scales around 1/sqrt(d): across the 4-/8-wave threshold, ragged
+    tails and the split paths."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        nseg = int(rng.integers(1, 5))
+        kind = rng.choice(3, size=nseg, p=[0.15, 0.25, 0.6])  # empty, short, longer
+        lengths = [0 if k == 0 else int(rng.integers(1, 65)) if k == 1 else
+                   int(rng.integers(65, 3001)) for k in kind]
+        if sum(lengths) == 0:
+            lengths[0] = 1
+        hkv = int(rng.choice([1, 2, 3]))
+        hq = hkv * int(rng.choice([1, 2, 4]))
+        d = int(rng.choice([64, 128]))
+        causal = bool(rng.integers(0, 2))
+        scale = float(rng.uniform(0.6, 1.4) / math.sqrt(d))
+        cases.append((lengths, hq, hkv, d, causal, scale))
+    return cases
+
+
+@pytest.mark.parametrize("lengths,hq,hkv,d,causal,scale", _random_shapes())
+def test_random_shapes_full_parity(lengths, hq, hkv, d, causal, scale):
+    _full_parity(lengths, hq, hkv, d, causal, scale)
+
+
 @pytest.mark.parametrize("lengths,hq,hkv,d,causal", [
     ([3000], 2, 1, 128, True),        # 8-wave forward
     ([1500, 700], 2, 2, 64, True),    # 4-wave forward
