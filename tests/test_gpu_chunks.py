@@ -157,6 +157,69 @@ def test_chunk_gradients(T, hq, hkv, d, causal, cuts):
     check_close("dV", dv.double().cpu().numpy(), dV)
 
 
+def _random_pairs(n=20, seed=13198):
+    """Seeded random (query chunk, key chunk) pairs of one sequence of 64-5,000
+    tokens: chunks of 1-3,000 rows anywhere (before, across or after each
+    other, empty key chunks included), 1-3 kv heads in groups of 1, 2 or 4,
+    d in {64, 128}, either causal flag."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        T = int(rng.integers(64, 5001))
+        qa = int(rng.integers(0, T))
+        qb = int(rng.integers(qa + 1, min(T, qa + 3000) + 1))
+        ka = int(rng.integers(0, T))
+        kb = ka if rng.random() < 0.1 else int(rng.integers(ka + 1, min(T, ka + 3000) + 1))
+        hkv = int(rng.choice([1, 2, 3]))
+        hq = hkv * int(rng.choice([1, 2, 4]))
+        cases.append((T, hq, hkv, int(rng.choice([64, 128])), bool(rng.integers(0, 2)),
+                      (qa, qb), (ka, kb)))
+    return cases
+
+
+@pytest.mark.parametrize("T,hq,hkv,d,causal,qs,ks", _random_pairs())
+def test_random_chunk_pairs(T, hq, hkv, d, causal, qs, ks):
+    """Partial forward and the pair's gradient contribution of random chunk
+    pairs against the oracle's (O and LSE fed to the backward are the
+    oracle's final ones over the whole sequence, rounded as the device
+    stores them)."""
+    import torch
+    from paper_2511_13198_amd import pdyattn
+    bits, f = _host(T, hq, hkv, d, 17)
+    scale = 1.0 / np.sqrt(d)
+    (qa, qb), (ka, kb) = qs, ks
+    log(f"  T={T} chunk q[{qa},{qb}) k[{ka},{kb}) Hq={hq} Hkv={hkv} d={d} causal={causal}")
+    o_ref, l_ref = ora.partial_forward(f["q"][qa:qb], f["k"][ka:kb], f["v"][ka:kb], qa, ka,
+                                       causal, scale)
+    q, do = _dev(bits, "q", qa, qb), _dev(bits, "do", qa, qb)
+    if kb > ka:
+        k, v = _dev(bits, "k", ka, kb), _dev(bits, "v", ka, kb)
+    else:  # an empty key chunk
+        k = v = torch.empty((0, hkv, d), dtype=torch.bfloat16, device="cuda")
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((hq, qb - qa), float("nan"), dtype=torch.float32, device=q.device)
+    pdyattn.attn_fwd_chunk(q, k, v, qa, ka, causal, scale, out=o, lse=lse)
+    torch.cuda.synchronize()
+    _check_partial("O", "LSE", o.double().cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref)
+    if kb == ka:
+        return
+    O, L = ora.forward(f["q"], f["k"], f["v"], np.array([0, T]), causal, scale)
+    o_bits = wl.f32_to_bf16_bits(O[qa:qb].astype(np.float32))
+    l32 = np.ascontiguousarray(L[:, qa:qb].astype(np.float32))
+    gq, gk, gv = pdyattn.attn_bwd_chunk(q, k, v, to_device_bf16(o_bits),
+                                        torch.from_numpy(l32).cuda(), do, qa, ka, causal, scale)
+    torch.cuda.synchronize()
+    rq, rk, rv = ora.partial_backward(f["q"][qa:qb], f["k"][ka:kb], f["v"][ka:kb],
+                                      wl.bf16_bits_to_f64(o_bits), l32.astype(np.float64),
+                                      f["do"][qa:qb], qa, ka, causal, scale)
+    for nm, g, r in (("dQc", gq, rq), ("dKc", gk, rk), ("dVc", gv, rv)):
+        gn = g.double().cpu().numpy()
+        if not np.any(r):
+            assert not np.any(gn), f"{nm}: nonzero gradient for an invisible pair"
+        else:
+            check_close(nm, gn, r)
+
+
 def test_merge_against_the_oracle():
     import torch
     from paper_2511_13198_amd import pdyattn
