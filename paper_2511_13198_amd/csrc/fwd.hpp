@@ -334,19 +334,21 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
       const bool more = tn < t_end;
       if (active(it)) {
         // the copies of tile tn go out one per K-step of S, so that they
-        // trickle into the memory pipeline instead of queueing at once
-        // (built for every tile; only used when there is a next one)
+        // trickle into the memory pipeline instead of queueing at once;
+        // past the last tile they get an empty range (they fetch nothing and
+        // fill the free stage with zeros), so that no branch surrounds them
         const int kt = k_lo + tn * BK;
-        const auto rsk = TileDma<KL, BK, NW>::src(kbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
-        const auto rsv = TileDma<VL, BK, NW>::src(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
+        const int rows_next = more ? k_hi - kt : 0;
+        const auto rsk = TileDma<KL, BK, NW>::src(kbase + (size_t)kt * kvstride, kvstride, rows_next);
+        const auto rsv = TileDma<VL, BK, NW>::src(vbase + (size_t)kt * kvstride, kvstride, rows_next);
         uint16_t* kl = kbuf(tn);
         uint16_t* vl = vbuf(tn);
         auto copy = [&](auto CI) __attribute__((always_inline)) {
           constexpr int c = decltype(CI)::value;
           if constexpr (c < PK) {
-            if (more) kd.issue_one(c, rsk, kl);
+            kd.issue_one(c, rsk, kl);
           } else if constexpr (c < PK + PV) {
-            if (more) vd.issue_one(c - PK, rsv, vl);
+            vd.issue_one(c - PK, rsv, vl);
           }
         };
         // the tile is taken in softmax steps of BKS keys; the first step
@@ -371,6 +373,8 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
         issue(tn);
       }
     }
+    // the last tile's empty-range copies land before the workgroup ends
+    wait_dma();
   }
 
   fwd_epilogue<D>(a, oacc, m, lsum, row, seg_hi, h, part, hh);
