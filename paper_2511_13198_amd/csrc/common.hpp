@@ -304,7 +304,9 @@ struct TileDma {
   // copies over the products of a step instead of queueing them all at once.
   __device__ __forceinline__ void issue_one(int i, const Src& s, uint16_t* lds) const {
     const int k = wave + NW * i;
-    if (INSTS % NW != 0 && k >= INSTS) return;  // wave-uniform
+    // only a wave's last copy can lie past the tile (NW * (PER_WAVE - 1) <
+    // INSTS), so the check folds away for the others once i is a constant
+    if (INSTS % NW != 0 && i == PER_WAVE - 1 && k >= INSTS) return;  // wave-uniform
     copy(s, voff[i], lds + k * 512);
   }
   // All of this wave's copies of the tile (valid_rows >= 1).
@@ -314,7 +316,7 @@ struct TileDma {
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i) {
       const int k = wave + NW * i;
-      if (INSTS % NW != 0 && k >= INSTS) break;  // wave-uniform
+      if (INSTS % NW != 0 && i == PER_WAVE - 1 && k >= INSTS) break;  // wave-uniform
       copy(s, voff[i], lds + k * 512);
     }
   }

@@ -343,12 +343,15 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
         const auto rsv = TileDma<VL, BK, NW>::src(vbase + (size_t)kt * kvstride, kvstride, rows_next);
         uint16_t* kl = kbuf(tn);
         uint16_t* vl = vbuf(tn);
+        // V's copies first: every wave has the same number of them, while a
+        // wave's last K copy may lie past the tile and sits behind a branch,
+        // which is then outside the K-steps of S
         auto copy = [&](auto CI) __attribute__((always_inline)) {
           constexpr int c = decltype(CI)::value;
-          if constexpr (c < PK) {
-            kd.issue_one(c, rsk, kl);
-          } else if constexpr (c < PK + PV) {
-            vd.issue_one(c - PK, rsv, vl);
+          if constexpr (c < PV) {
+            vd.issue_one(c, rsv, vl);
+          } else if constexpr (c < PV + PK) {
+            kd.issue_one(c - PV, rsk, kl);
           }
         };
         // the tile is taken in softmax steps of BKS keys; the first step
