@@ -390,18 +390,24 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
       if (more) load_stat(nxt);
       // the next step's copies go out one per K-step of the first half's
       // S/dP, so that they trickle into the memory pipeline instead of
-      // stalling every wave at once (built for every step; only used when
-      // there is a next one)
-      const int rvn = rows_valid(nxt);
+      // stalling every wave at once; past the last step they get an empty
+      // range (they fetch nothing and fill the free stage's Q and dO tiles
+      // with zeros), so that no branch surrounds them
+      const int rvn = more ? rows_valid(nxt) : 0;
       const typename QD::Src rsq = QD::src(row_ptr(a.q, nxt), qstride, rvn);
       const typename QD::Src rsg = QD::src(row_ptr(a.dout, nxt), qstride, rvn);
       const int bn = (step + 1) & 1;
+      // every wave has PQ - 1 copies of each tile; a wave's last one may lie
+      // past the tile (a branch), so those two go out at the last K-step
       const bool ran = compute(step, cur, 0, [&](auto KS) __attribute__((always_inline)) {
         constexpr int c = decltype(KS)::value;
-        if constexpr (c < PQ) {
-          if (more) qd.issue_one(c, rsq, qbuf(bn));
-        } else if constexpr (c < 2 * PQ) {
-          if (more) qd.issue_one(c - PQ, rsg, gbuf(bn));
+        if constexpr (c < PQ - 1) {
+          qd.issue_one(c, rsq, qbuf(bn));
+        } else if constexpr (c < 2 * (PQ - 1)) {
+          qd.issue_one(c - (PQ - 1), rsg, gbuf(bn));
+        } else if constexpr (c == D / 16 - 1) {
+          qd.issue_one(PQ - 1, rsq, qbuf(bn));
+          qd.issue_one(PQ - 1, rsg, gbuf(bn));
         }
       });
       if (!ran && more) issue(step + 1, nxt);
@@ -632,21 +638,29 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
       const bool more = it + 1 < t_end;
       wait_dma();
       __syncthreads();
-      // (built for every tile; only used when there is a next one)
+      // past the last tile the copies get an empty range (they fetch
+      // nothing and fill the free stage with zeros), so that no branch
+      // surrounds them; a wave's last V copy may lie past the tile (a
+      // branch), so it goes out at the tile's last K-step
       const int kt = k_lo + (it + 1) * BK;
-      const typename KD::Src rsk = KD::src(kbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
-      const typename VD::Src rsv = VD::src(vbase + (size_t)kt * kvstride, kvstride, k_hi - kt);
+      const int rows_next = more ? k_hi - kt : 0;
+      const typename KD::Src rsk = KD::src(kbase + (size_t)kt * kvstride, kvstride, rows_next);
+      const typename VD::Src rsv = VD::src(vbase + (size_t)kt * kvstride, kvstride, rows_next);
       const int bn = (it + 1) & 1;
       const bool ran = compute(it, [&](auto N) __attribute__((always_inline)) {
         constexpr int n = decltype(N)::value;
         if constexpr (n % GAP == 0 && n / GAP < PK) {
-          if (more) kd.issue_one(n / GAP, rsk, kbuf(bn));
-        } else if constexpr (n % GAP == 0 && n / GAP < NCOPY) {
-          if (more) vd.issue_one(n / GAP - PK, rsv, vbuf(bn));
+          kd.issue_one(n / GAP, rsk, kbuf(bn));
+        } else if constexpr (n % GAP == 0 && n / GAP < NCOPY - 1) {
+          vd.issue_one(n / GAP - PK, rsv, vbuf(bn));
+        } else if constexpr (n == (BK / 32) * (D / 16) - 1) {
+          vd.issue_one(NCOPY - 1 - PK, rsv, vbuf(bn));
         }
       });
       if (!ran && more) issue(it + 1);
     }
+    // the last tile's empty-range copies land before the workgroup ends
+    wait_dma();
   }
 
   if (row < seg_hi) {
