@@ -361,17 +361,23 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
           const int k0s = k_lo + it * BK + sub * BKS;
           if (sub == 0 || (k0s < kv_end && (!a.causal || k0s <= wrow_last + shift))) {
             compute_s(kbuf(it) + sub * BKS * KL::ROW, [&](auto KS) __attribute__((always_inline)) {
-              if constexpr (sub == 0) copy(KS);
+              if constexpr (sub == 0) {
+                constexpr int ks = decltype(KS)::value;
+                if constexpr (ks < PK + PV - 1) copy(KS);
+                // the other copies that every wave has go out with the last
+                // K-step
+                if constexpr (ks == D / 16 - 1)
+                  static_for<PK + PV - 1>([&](auto CI) {
+                    if constexpr (decltype(CI)::value >= D / 16) copy(CI);
+                  });
+              }
             });
             softmax_pv(k0s, vbuf(it) + sub * BKS * VL::ROW);
           }
-          if constexpr (sub == 0) {
-            // copies beyond one per K-step
-            static_for<PK + PV>([&](auto CI) {
-              if constexpr (decltype(CI)::value >= D / 16) copy(CI);
-            });
-          }
         });
+        // a wave's last K copy (which may lie past the tile: a branch) at
+        // the end of the tile
+        copy(std::integral_constant<int, PK + PV - 1>{});
       } else if (more) {
         issue(tn);
       }
