@@ -170,7 +170,7 @@ __global__ void __launch_bounds__(512) bwd_dkdv_kernel(BwdArgs a) {
   const int g = a.hq / a.hkv;
 
   const int l = __lane_id();
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int hh = l >> 5;
   const int kw0 = k0 + w * 32;    // first key of this wave
   const int key = kw0 + (l & 31);  // this lane's key
@@ -485,7 +485,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) bwd_dq_kernel(BwdArg
   const int hk = h / (a.hq / a.hkv);
 
   const int l = __lane_id();
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int hh = l >> 5;
   const int row = q0 + w * 32 + (l & 31);
   const int wrow0 = q0 + w * 32;

@@ -160,7 +160,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
   const int hk = h / (a.hq / a.hkv);
 
   const int l = __lane_id();
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int hh = l >> 5;
   const int row = q0 + w * 32 + (l & 31);  // this lane's query row
   const int wrow0 = q0 + w * 32;
