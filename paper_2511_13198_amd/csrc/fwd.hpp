@@ -287,6 +287,10 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
     constexpr int NDB = D / 32, NT16 = BKS / 16;
     const uint32_t va = lds_addr(vtile) + v_lane * 2;
     TrRegs vr[2][NDB];  // step T uses vr[T & 1]; no copies of in-flight registers
+    // priority for the wave while it issues these products, as in the
+    // backward's product phases (forward 0.8 % faster; in the S^T products
+    // it is 1.6 % slower)
+    __builtin_amdgcn_s_setprio(1);
     static_for<NDB>([&](auto DB) { tr_issue<VL, 0, DB * 32>(va, vr[0][DB]); });
     static_for<NT16>([&](auto T) {
       constexpr int cur = T & 1;
@@ -300,6 +304,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) fwd_kernel(FwdArgs a
 #pragma unroll
       for (int db = 0; db < NDB; ++db) oacc[db] = mfma32(vr[cur][db].operand(), pf, oacc[db]);
     });
+    __builtin_amdgcn_s_setprio(0);
   };
 
   const uint16_t* kbase = a.k + (size_t)hk * D;
